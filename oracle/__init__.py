@@ -1,0 +1,300 @@
+"""CPU oracle of the data-collection step -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, single-threaded C (``rlsim_oracle.c``) behind a ctypes wrapper.
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The GPU library never loads it, and it
+shares no code with the GPU library: its configuration struct, constants and
+RNG are declared here and in ``rlsim_oracle.c`` independently.
+
+What it computes (one cart-pole environment per array column, Background,
+"Cartpole Simulator"; the simulation/inference loop of Background, "RL
+Training"; K steps per call as in "Simulator Kernel Fusion"):
+
+* ``philox4x32_10`` -- the counter-based generator of Salmon et al. (SC'11).
+* ``cartpole_step`` -- one explicit-Euler step of the frictionless cart and
+  uniform rod, fp32, each operation rounded once.
+* ``Sim`` -- N environments with auto-reset, the random-action or MLP-policy
+  loop, padding words (the paper's state-size factor S, Simulator Complexity)
+  and per-256-env block statistics.
+
+Parity pins live in ``tests/test_oracle_*.py``.  Functions without an
+independent pin: none.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "rlsim_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-Wall"]
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no contraction, no fast-math)."""
+    tmp = _LIB_PATH + ".tmp"
+    subprocess.run(["gcc", *_CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class Params(ctypes.Structure):
+    """Simulator configuration; field meaning as documented in rlsim_oracle.c."""
+
+    _fields_ = [
+        ("gravity", ctypes.c_float), ("masscart", ctypes.c_float), ("masspole", ctypes.c_float),
+        ("half_length", ctypes.c_float), ("force_mag", ctypes.c_float), ("tau", ctypes.c_float),
+        ("x_threshold", ctypes.c_float), ("theta_threshold_rad", ctypes.c_float),
+        ("max_episode_steps", ctypes.c_uint32),
+        ("reset_low", ctypes.c_float), ("reset_high", ctypes.c_float),
+        ("pad_a_low", ctypes.c_float), ("pad_a_high", ctypes.c_float),
+        ("pad_b_low", ctypes.c_float), ("pad_b_high", ctypes.c_float),
+        ("no_termination", ctypes.c_uint32),
+    ]
+
+
+class _Policy(ctypes.Structure):
+    _fields_ = [("bf16", ctypes.c_int)] + [
+        (name, ctypes.POINTER(ctypes.c_float)) for name in ("w1", "b1", "w2", "b2", "w3", "b3")
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load (building first if needed) the oracle shared library."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build()
+    L = ctypes.CDLL(_LIB_PATH)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    f32p = ctypes.POINTER(ctypes.c_float)
+    L.orc_philox4x32_10.argtypes = [u32p, u32p, u32p]
+    L.orc_philox4x32_10.restype = None
+    L.orc_u24.argtypes = [ctypes.c_uint32]
+    L.orc_u24.restype = ctypes.c_float
+    L.orc_uniform.argtypes = [ctypes.c_uint32, ctypes.c_float, ctypes.c_float]
+    L.orc_uniform.restype = ctypes.c_float
+    L.orc_sin.argtypes = [ctypes.c_float]
+    L.orc_sin.restype = ctypes.c_float
+    L.orc_cos.argtypes = [ctypes.c_float]
+    L.orc_cos.restype = ctypes.c_float
+    L.orc_cartpole_step.argtypes = [ctypes.POINTER(Params), f32p, ctypes.c_int, f32p]
+    L.orc_cartpole_step.restype = None
+    L.orc_terminated.argtypes = [ctypes.POINTER(Params), f32p]
+    L.orc_terminated.restype = ctypes.c_int
+    L.orc_reset_draw.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, f32p]
+    L.orc_reset_draw.restype = None
+    L.orc_action_bit.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32]
+    L.orc_action_bit.restype = ctypes.c_int
+    L.orc_policy_u.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32]
+    L.orc_policy_u.restype = ctypes.c_float
+    L.orc_pad_params.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, f32p, f32p]
+    L.orc_pad_params.restype = None
+    L.orc_pad_update.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int]
+    L.orc_pad_update.restype = ctypes.c_float
+    L.orc_round_bf16.argtypes = [ctypes.c_double]
+    L.orc_round_bf16.restype = ctypes.c_double
+    L.orc_mlp_p0.argtypes = [ctypes.POINTER(_Policy), f32p]
+    L.orc_mlp_p0.restype = ctypes.c_double
+    L.orc_create.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(Params)]
+    L.orc_create.restype = ctypes.c_void_p
+    L.orc_destroy.argtypes = [ctypes.c_void_p]
+    L.orc_destroy.restype = None
+    L.orc_reset.argtypes = [ctypes.c_void_p, ctypes.c_uint64]
+    L.orc_reset.restype = None
+    L.orc_step.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(_Policy),
+                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_void_p]
+    L.orc_step.restype = ctypes.c_int
+    L.orc_get_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint64)]
+    L.orc_get_state.restype = None
+    L.orc_set_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+    L.orc_set_state.restype = ctypes.c_int
+    L.orc_get_pad_params.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    L.orc_get_pad_params.restype = None
+    _lib = L
+    return L
+
+
+def make_params(**overrides) -> Params:
+    """Params from keyword values (every field must be given)."""
+    p = Params()
+    names = [f[0] for f in Params._fields_]
+    missing = [n for n in names if n not in overrides]
+    if missing:
+        raise ValueError(f"missing oracle parameters: {missing}")
+    for k, v in overrides.items():
+        if k not in names:
+            raise ValueError(f"unknown oracle parameter {k}")
+        setattr(p, k, v)
+    return p
+
+
+def _u32(a):
+    return np.ascontiguousarray(a, dtype=np.uint32)
+
+
+def philox4x32_10(counter, key) -> np.ndarray:
+    """Philox4x32-10 of one (counter[4], key[2]) pair -> 4 uint32 words."""
+    c = _u32(counter)
+    k = _u32(key)
+    out = np.zeros(4, dtype=np.uint32)
+    P = ctypes.POINTER(ctypes.c_uint32)
+    lib().orc_philox4x32_10(c.ctypes.data_as(P), k.ctypes.data_as(P), out.ctypes.data_as(P))
+    return out
+
+
+def u24(r: int) -> float:
+    return float(np.float32(lib().orc_u24(int(r))))
+
+
+def uniform(r: int, lo: float, hi: float) -> np.float32:
+    return np.float32(lib().orc_uniform(int(r), lo, hi))
+
+
+def sin_poly(th: float) -> np.float32:
+    return np.float32(lib().orc_sin(float(np.float32(th))))
+
+
+def cos_poly(th: float) -> np.float32:
+    return np.float32(lib().orc_cos(float(np.float32(th))))
+
+
+def cartpole_step(params: Params, state, action: int) -> np.ndarray:
+    """One Euler step from a 4-float state; returns the next 4 floats."""
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    out = np.zeros(4, dtype=np.float32)
+    P = ctypes.POINTER(ctypes.c_float)
+    lib().orc_cartpole_step(ctypes.byref(params), s.ctypes.data_as(P), int(action), out.ctypes.data_as(P))
+    return out
+
+
+def terminated(params: Params, state) -> bool:
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    return bool(lib().orc_terminated(ctypes.byref(params), s.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+
+
+def reset_draw(params: Params, seed: int, env: int, t: int) -> np.ndarray:
+    out = np.zeros(4, dtype=np.float32)
+    lib().orc_reset_draw(ctypes.byref(params), seed, env, t, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
+    return out
+
+
+def action_bit(seed: int, env: int, t: int) -> int:
+    return int(lib().orc_action_bit(seed, env, t))
+
+
+def policy_u(seed: int, env: int, t: int) -> np.float32:
+    return np.float32(lib().orc_policy_u(seed, env, t))
+
+
+def pad_params(params: Params, seed: int, env: int, j: int):
+    a = ctypes.c_float()
+    b = ctypes.c_float()
+    lib().orc_pad_params(ctypes.byref(params), seed, env, j, ctypes.byref(a), ctypes.byref(b))
+    return np.float32(a.value), np.float32(b.value)
+
+
+def pad_update(s: float, a: float, b: float, u: int) -> np.float32:
+    return np.float32(lib().orc_pad_update(float(s), float(a), float(b), int(u)))
+
+
+def round_bf16(v: float) -> float:
+    return float(lib().orc_round_bf16(float(v)))
+
+
+class Policy:
+    """MLP weights (fp32 numpy, row-major [out][in]) for the oracle."""
+
+    def __init__(self, w1, b1, w2, b2, w3, b3, bf16: bool = False):
+        self._arrs = [None if x is None else np.ascontiguousarray(x, dtype=np.float32)
+                      for x in (w1, b1, w2, b2, w3, b3)]
+        shapes = [(64, 4), (64,), (64, 64), (64,), (2, 64), (2,)]
+        for a, shp in zip(self._arrs, shapes):
+            if a is not None and a.shape != shp:
+                raise ValueError(f"policy array shape {a.shape} != {shp}")
+        for i in (0, 2, 4):
+            if self._arrs[i] is None:
+                raise ValueError("weights may not be None")
+        P = ctypes.POINTER(ctypes.c_float)
+        self.struct = _Policy(int(bool(bf16)), *[
+            ctypes.cast(None, P) if a is None else a.ctypes.data_as(P) for a in self._arrs])
+
+    def p0(self, obs) -> float:
+        o = np.ascontiguousarray(obs, dtype=np.float32)
+        return float(lib().orc_mlp_p0(ctypes.byref(self.struct), o.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+
+
+class Sim:
+    """A slice of environments with global ids env0 .. env0+n-1."""
+
+    def __init__(self, n_envs: int, D: int, params: Params, env0: int = 0):
+        self.n, self.D, self.env0 = int(n_envs), int(D), int(env0)
+        self.params = params
+        self._h = lib().orc_create(self.n, self.env0, self.D, ctypes.byref(params))
+        if not self._h:
+            raise MemoryError("orc_create failed")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            lib().orc_destroy(h)
+            self._h = None
+
+    @property
+    def n_blocks(self) -> int:
+        return (self.env0 + self.n - 1) // 256 - self.env0 // 256 + 1
+
+    def reset(self, seed: int) -> None:
+        lib().orc_reset(self._h, int(seed))
+
+    def step(self, K: int, policy: Policy | None = None, record: bool = True, stats: bool = True):
+        """Run K steps; returns dict of trajectory arrays (or {} if not record)."""
+        n = self.n
+        out = {}
+        ptr = lambda a: a.ctypes.data if a is not None else None  # noqa: E731
+        if record:
+            out["obs"] = np.empty((K, 4, n), dtype=np.float32)
+            out["action"] = np.empty((K, n), dtype=np.uint8)
+            out["reward"] = np.empty((K, n), dtype=np.float32)
+            out["done"] = np.empty((K, n), dtype=np.uint8)
+            if policy is not None:
+                out["p0"] = np.empty((K, n), dtype=np.float64)
+        if stats:
+            out["stats"] = np.empty((self.n_blocks, 4), dtype=np.uint32)
+        rc = lib().orc_step(self._h, int(K), ctypes.byref(policy.struct) if policy is not None else None,
+                            ptr(out.get("obs")), ptr(out.get("action")), ptr(out.get("reward")),
+                            ptr(out.get("done")), ptr(out.get("stats")), ptr(out.get("p0")))
+        if rc != 0:
+            raise RuntimeError(f"orc_step failed ({rc})")
+        return out
+
+    def get_state(self):
+        st = np.empty((4 + self.D, self.n), dtype=np.float32)
+        ep = np.empty(self.n, dtype=np.uint32)
+        t = ctypes.c_uint64()
+        lib().orc_get_state(self._h, st.ctypes.data, ep.ctypes.data, ctypes.byref(t))
+        return st, ep, int(t.value)
+
+    def set_state(self, state, ep, t: int) -> None:
+        st = np.ascontiguousarray(state, dtype=np.float32)
+        e = np.ascontiguousarray(ep, dtype=np.uint32)
+        if st.shape != (4 + self.D, self.n) or e.shape != (self.n,):
+            raise ValueError("state shape mismatch")
+        rc = lib().orc_set_state(self._h, st.ctypes.data, e.ctypes.data, int(t))
+        if rc != 0:
+            raise RuntimeError(f"orc_set_state failed ({rc})")
+
+    def pad_params(self):
+        a = np.empty((self.D, self.n), dtype=np.float32)
+        b = np.empty((self.D, self.n), dtype=np.float32)
+        lib().orc_get_pad_params(self._h, a.ctypes.data, b.ctypes.data)
+        return a, b

@@ -1,0 +1,468 @@
+/*
+ * rlsim_oracle.c -- TEST INFRASTRUCTURE ONLY.
+ *
+ * The plain, slow, single-threaded CPU definition of the data-collection step
+ * of "Optimizing Data Collection in Deep Reinforcement Learning" (Gleeson et
+ * al., 2022): N independent cart-pole simulators (Background, "Cartpole
+ * Simulator") driven by a simulation/inference loop for K steps (Background,
+ * "RL Training", and the data-collection figure).  The GPU library is checked
+ * against this file; nothing in the product links, loads or runs it.  Only the
+ * tests, the smoke check and the benchmark's CPU-baseline leg may use it.
+ *
+ * It shares no code, header or constant table with the HIP path.  Every
+ * function below is written in the order of the definitions it follows, one
+ * IEEE operation per line where rounding matters, so that a reader can check
+ * it against the stated equations by eye.  Build: gcc -O2 -ffp-contract=off
+ * (no fast-math, no FTZ): every fp32 product, sum and fmaf is rounded exactly
+ * once, round-to-nearest-even.
+ *
+ * The paper gives no equations, constants, reward, reset rule or RNG; the
+ * readings used here (cart + uniform rod, explicit Euler, Philox4x32-10 with a
+ * block-grouped counter, strict thresholds, auto-reset) are the ones listed in
+ * the design notes.  Parity of every function is pinned by the CPU tests
+ * (known-answer Philox words, hand-derived rational cart-pole steps, a
+ * 50-digit Euler-Lagrange solve, linearisation, conservation laws, closed
+ * forms of the padding recurrence and of special MLP weights).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As   */
+/* Easy as 1, 2, 3", SC'11): ten rounds of a 4-word multiply/xor bijection    */
+/* with a Weyl-sequence key schedule.                                        */
+/* ------------------------------------------------------------------------ */
+void orc_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint32_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c1 ^ k0;
+        uint32_t n1 = lo1;
+        uint32_t n2 = hi0 ^ c3 ^ k1;
+        uint32_t n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+        k0 += 0x9E3779B9u; /* the key bump after round 10 is never used */
+        k1 += 0xBB67AE85u;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Stream ids of the counter (third counter word). */
+enum { ORC_STREAM_RESET = 0, ORC_STREAM_ACTION = 1, ORC_STREAM_PARAMS = 2, ORC_STREAM_POLICY = 3 };
+
+static void orc_draw(uint64_t seed, uint32_t env, uint32_t block, uint32_t stream, uint32_t out[4])
+{
+    uint32_t ctr[4] = { env, block, stream, 0u };
+    uint32_t key[2] = { (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32) };
+    orc_philox4x32_10(ctr, key, out);
+}
+
+/* Top 24 bits of a word as a float in [0, 1 - 2^-24]; exact. */
+float orc_u24(uint32_t r)
+{
+    float m = (float)(r >> 8);
+    return m * 0x1.0p-24f;
+}
+
+/* uniform on [lo, hi): lo + u24 * (hi - lo), the product-sum rounded once. */
+float orc_uniform(uint32_t r, float lo, float hi)
+{
+    float width = hi - lo;
+    return fmaf(orc_u24(r), width, lo);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Configuration (same meaning as the library's, declared independently).    */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    float gravity, masscart, masspole, half_length, force_mag, tau;
+    float x_threshold, theta_threshold_rad;
+    uint32_t max_episode_steps;      /* 0 = no time limit */
+    float reset_low, reset_high;
+    float pad_a_low, pad_a_high, pad_b_low, pad_b_high;
+    uint32_t no_termination;         /* nonzero: termination never fires */
+} orc_params;
+
+/* ------------------------------------------------------------------------ */
+/* Truncated Maclaurin series for sin and cos, Horner form with fmaf.        */
+/* Used for |theta| <= 12 degrees (every pre-step state of a live episode),  */
+/* where the truncation error is below 1e-15.                                */
+/* ------------------------------------------------------------------------ */
+float orc_sin(float th)
+{
+    const float s3 = (float)(-1.0 / 6.0);
+    const float s5 = (float)(1.0 / 120.0);
+    const float s7 = (float)(-1.0 / 5040.0);
+    const float s9 = (float)(1.0 / 362880.0);
+    float z = th * th;
+    float q = fmaf(s9, z, s7);
+    q = fmaf(q, z, s5);
+    q = fmaf(q, z, s3);
+    float th3 = th * z;
+    return fmaf(th3, q, th);          /* th + th^3 (s3 + s5 z + s7 z^2 + s9 z^3) */
+}
+
+float orc_cos(float th)
+{
+    const float c2 = -0.5f;
+    const float c4 = (float)(1.0 / 24.0);
+    const float c6 = (float)(-1.0 / 720.0);
+    const float c8 = (float)(1.0 / 40320.0);
+    float z = th * th;
+    float q = fmaf(c8, z, c6);
+    q = fmaf(q, z, c4);
+    q = fmaf(q, z, c2);
+    return fmaf(z, q, 1.0f);          /* 1 + z (c2 + c4 z + c6 z^2 + c8 z^3) */
+}
+
+/* ------------------------------------------------------------------------ */
+/* One explicit-Euler step of the frictionless cart + uniform rod.           */
+/*   Lagrangian L = 1/2 M xd^2 + m l xd thd cos th + 2/3 m l^2 thd^2         */
+/*                  - m g l cos th      (M = cart + pole mass, l = half len) */
+/*   => thacc = (g sin th - cos th * temp) / (l (4/3 - m cos^2 th / M)),     */
+/*      temp  = (F + m l thd^2 sin th) / M,                                  */
+/*      xacc  = temp - m l thacc cos th / M.                                 */
+/* Positions advance with the old velocities.  a == 1 pushes towards +x.     */
+/* ------------------------------------------------------------------------ */
+void orc_cartpole_step(const orc_params* p, const float in[4], int action, float out[4])
+{
+    /* derived constants, one fp32 operation each */
+    float total_mass = p->masscart + p->masspole;
+    float pole_ml = p->masspole * p->half_length;
+    float inv_total = 1.0f / total_mass;
+    float m_over_M = p->masspole * inv_total;
+    float ml_over_M = pole_ml * inv_total;
+    float four_thirds = 4.0f / 3.0f;
+
+    float x = in[0], xd = in[1], th = in[2], thd = in[3];
+    float force = action ? p->force_mag : -p->force_mag;
+
+    float sin_th = orc_sin(th);
+    float cos_th = orc_cos(th);
+
+    float thd2 = thd * thd;
+    float ml_thd2 = pole_ml * thd2;
+    float f_plus = fmaf(ml_thd2, sin_th, force);        /* F + m l thd^2 sin th */
+    float temp = f_plus * inv_total;
+
+    float g_sin = p->gravity * sin_th;
+    float num = fmaf(-cos_th, temp, g_sin);             /* g sin th - cos th temp */
+    float cos2 = cos_th * cos_th;
+    float bracket = fmaf(-m_over_M, cos2, four_thirds); /* 4/3 - m cos^2 th / M */
+    float den = p->half_length * bracket;
+    float thacc = num / den;
+
+    float k_th = ml_over_M * thacc;
+    float xacc = fmaf(-k_th, cos_th, temp);             /* temp - m l thacc cos th / M */
+
+    out[0] = fmaf(p->tau, xd, x);
+    out[1] = fmaf(p->tau, xacc, xd);
+    out[2] = fmaf(p->tau, thd, th);
+    out[3] = fmaf(p->tau, thacc, thd);
+}
+
+/* Strict threshold test on the post-step state; NaN compares false. */
+int orc_terminated(const orc_params* p, const float s[4])
+{
+    if (p->no_termination) return 0;
+    float x = s[0], th = s[2];
+    return (x < -p->x_threshold) || (x > p->x_threshold) ||
+           (th < -p->theta_threshold_rad) || (th > p->theta_threshold_rad);
+}
+
+/* Initial state of an episode that begins at global step t: stream RESET,  */
+/* counter block t/4, words 0..3 -> x, xd, th, thd.                          */
+void orc_reset_draw(const orc_params* p, uint64_t seed, uint32_t env, uint32_t t, float out[4])
+{
+    uint32_t w[4];
+    orc_draw(seed, env, t >> 2, ORC_STREAM_RESET, w);
+    for (int c = 0; c < 4; ++c) out[c] = orc_uniform(w[c], p->reset_low, p->reset_high);
+}
+
+/* Random action at global step t: stream ACTION, counter block t/128,      */
+/* bit (t mod 32) of word ((t/32) mod 4).                                    */
+int orc_action_bit(uint64_t seed, uint32_t env, uint32_t t)
+{
+    uint32_t w[4];
+    orc_draw(seed, env, t >> 7, ORC_STREAM_ACTION, w);
+    return (int)((w[(t >> 5) & 3u] >> (t & 31u)) & 1u);
+}
+
+/* Uniform used to sample the policy's action at step t: stream POLICY,     */
+/* counter block t/4, word (t mod 4).                                        */
+float orc_policy_u(uint64_t seed, uint32_t env, uint32_t t)
+{
+    uint32_t w[4];
+    orc_draw(seed, env, t >> 2, ORC_STREAM_POLICY, w);
+    return orc_u24(w[t & 3u]);
+}
+
+/* Padding-word parameters: stream PARAMS, counter block j.                  */
+void orc_pad_params(const orc_params* p, uint64_t seed, uint32_t env, uint32_t j, float* a, float* b)
+{
+    uint32_t w[4];
+    orc_draw(seed, env, j, ORC_STREAM_PARAMS, w);
+    *a = orc_uniform(w[0], p->pad_a_low, p->pad_a_high);
+    *b = orc_uniform(w[1], p->pad_b_low, p->pad_b_high);
+}
+
+/* One padding word: s <- a s + b u, rounded once (u is the action, 0 or 1). */
+float orc_pad_update(float s, float a, float b, int u)
+{
+    float bu = u ? b : 0.0f;
+    return fmaf(a, s, bu);
+}
+
+/* ------------------------------------------------------------------------ */
+/* MLP policy 4 -> 64 -> 64 -> 2, tanh hidden layers, weights row-major     */
+/* [out][in], evaluated in double.  p0 = softmax(logits)[0].                */
+/* bf16 mode rounds the weights, the input and both hidden activations to    */
+/* bfloat16 (round to nearest even) at the points where a bf16 kernel holds  */
+/* them; biases and sums stay in double.                                     */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    int bf16;
+    const float *w1, *b1, *w2, *b2, *w3, *b3;   /* biases may be NULL (zero) */
+} orc_policy;
+
+/* Round a double to the nearest bfloat16 value (ties to even), returned as */
+/* a double.  bfloat16 has an 8-bit significand and fp32's exponent range.  */
+double orc_round_bf16(double v)
+{
+    if (v != v || v == 0.0 || isinf(v)) return v;
+    int e;
+    frexp(v, &e);                               /* |v| = f 2^e, f in [0.5, 1) */
+    if (e < -125) e = -125;                     /* subnormal bf16 spacing      */
+    double q = ldexp(1.0, e - 8);               /* spacing of 8-bit significand */
+    double r = v / q;                           /* exact: power-of-two scale    */
+    double fl = floor(r);
+    double diff = r - fl;
+    double k;
+    if (diff > 0.5) k = fl + 1.0;
+    else if (diff < 0.5) k = fl;
+    else k = (fmod(fl, 2.0) == 0.0) ? fl : fl + 1.0;
+    double out = k * q;
+    if (fabs(out) > 3.3895313892515355e38) out = v > 0 ? INFINITY : -INFINITY;
+    return out;
+}
+
+static double orc_w(const orc_policy* pol, const float* w, int idx)
+{
+    double v = (double)w[idx];
+    return pol->bf16 ? orc_round_bf16(v) : v;
+}
+
+double orc_mlp_p0(const orc_policy* pol, const float obs[4])
+{
+    double in[4], h1[64], h2[64], logit[2];
+    for (int i = 0; i < 4; ++i) in[i] = pol->bf16 ? orc_round_bf16((double)obs[i]) : (double)obs[i];
+    for (int o = 0; o < 64; ++o) {
+        double acc = pol->b1 ? (double)pol->b1[o] : 0.0;
+        for (int i = 0; i < 4; ++i) acc += orc_w(pol, pol->w1, o * 4 + i) * in[i];
+        h1[o] = tanh(acc);
+        if (pol->bf16) h1[o] = orc_round_bf16(h1[o]);
+    }
+    for (int o = 0; o < 64; ++o) {
+        double acc = pol->b2 ? (double)pol->b2[o] : 0.0;
+        for (int i = 0; i < 64; ++i) acc += orc_w(pol, pol->w2, o * 64 + i) * h1[i];
+        h2[o] = tanh(acc);
+        if (pol->bf16) h2[o] = orc_round_bf16(h2[o]);
+    }
+    for (int o = 0; o < 2; ++o) {
+        double acc = pol->b3 ? (double)pol->b3[o] : 0.0;
+        for (int i = 0; i < 64; ++i) acc += orc_w(pol, pol->w3, o * 64 + i) * h2[i];
+        logit[o] = acc;
+    }
+    /* softmax over two logits: p0 = e^l0 / (e^l0 + e^l1) = 1 / (1 + e^(l1 - l0)) */
+    return 1.0 / (1.0 + exp(logit[1] - logit[0]));
+}
+
+/* ------------------------------------------------------------------------ */
+/* The vectorised simulator: a slice of n environments with global ids       */
+/* env0 .. env0+n-1, each with 4 cart-pole words, D padding words, and an    */
+/* episode step counter.  Host arrays, structure-of-arrays.                  */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    uint32_t n, env0, D;
+    orc_params p;
+    uint64_t seed;
+    uint32_t t;           /* global step of the next step */
+    int has_reset;
+    float* cart;          /* [4][n] */
+    uint32_t* ep;         /* [n]    steps taken in the current episode */
+    float* s;             /* [D][n] padding words */
+    float* a;             /* [D][n] */
+    float* b;             /* [D][n] */
+} orc_sim;
+
+void orc_destroy(orc_sim* sim)
+{
+    if (!sim) return;
+    free(sim->cart); free(sim->ep); free(sim->s); free(sim->a); free(sim->b);
+    free(sim);
+}
+
+orc_sim* orc_create(uint32_t n, uint32_t env0, uint32_t D, const orc_params* p)
+{
+    if (n == 0) return NULL;
+    orc_sim* sim = (orc_sim*)calloc(1, sizeof(orc_sim));
+    if (!sim) return NULL;
+    sim->n = n; sim->env0 = env0; sim->D = D; sim->p = *p;
+    sim->cart = (float*)calloc((size_t)4 * n, sizeof(float));
+    sim->ep = (uint32_t*)calloc(n, sizeof(uint32_t));
+    size_t nd = (size_t)D * n;
+    sim->s = (float*)calloc(nd ? nd : 1, sizeof(float));
+    sim->a = (float*)calloc(nd ? nd : 1, sizeof(float));
+    sim->b = (float*)calloc(nd ? nd : 1, sizeof(float));
+    if (!sim->cart || !sim->ep || !sim->s || !sim->a || !sim->b) { orc_destroy(sim); return NULL; }
+    return sim;
+}
+
+/* Every environment starts an episode at global step 0. */
+void orc_reset(orc_sim* sim, uint64_t seed)
+{
+    uint32_t n = sim->n;
+    sim->seed = seed;
+    sim->t = 0;
+    sim->has_reset = 1;
+    for (uint32_t i = 0; i < n; ++i) {
+        uint32_t env = sim->env0 + i;
+        float init[4];
+        orc_reset_draw(&sim->p, seed, env, 0u, init);
+        for (int c = 0; c < 4; ++c) sim->cart[(size_t)c * n + i] = init[c];
+        sim->ep[i] = 0;
+        for (uint32_t j = 0; j < sim->D; ++j) {
+            float a, b;
+            orc_pad_params(&sim->p, seed, env, j, &a, &b);
+            sim->a[(size_t)j * n + i] = a;
+            sim->b[(size_t)j * n + i] = b;
+            sim->s[(size_t)j * n + i] = 0.0f;
+        }
+    }
+}
+
+/*
+ * K steps of the data-collection loop for every environment of the slice.
+ * Step t of one environment:
+ *   obs   = the state before the step (recorded in the trajectory)
+ *   a_t   = policy ? (u_t < p0(obs) ? 0 : 1) : random action bit
+ *   next  = Euler step; padding words s <- a s + b a_t
+ *   n     = ep + 1; terminated = threshold crossed by next;
+ *   truncated = (max_episode_steps != 0 && n >= max_episode_steps)
+ *   done  = terminated | truncated << 1;  reward = 1
+ *   if done: the episode that begins at t+1 starts from the reset draw for
+ *            t+1, ep = 0, padding words = +0;  else ep = n.
+ * Outputs (each may be NULL), rows 0..K-1 of this call:
+ *   obs [K][4][n] f32, act [K][n] u8, rew [K][n] f32, done [K][n] u8,
+ *   p0 [K][n] f64 (policy runs), stats [nblk][4] u32 over 256-env blocks of
+ *   global env ids: {episodes finished, sum of their lengths, terminated,
+ *   truncated}; nblk = (env0+n-1)/256 - env0/256 + 1.
+ * Returns 0, or -1 before reset, -2 when t + K would pass 2^32 - 1.
+ */
+int orc_step(orc_sim* sim, uint32_t K, const orc_policy* pol,
+             float* obs, uint8_t* act, float* rew, uint8_t* done, uint32_t* stats, double* p0_out)
+{
+    if (!sim->has_reset) return -1;
+    if ((uint64_t)sim->t + (uint64_t)K > 0xFFFFFFFFull) return -2;
+    uint32_t n = sim->n;
+    uint32_t blk0 = sim->env0 / 256u;
+    if (stats) {
+        uint32_t nblk = (sim->env0 + n - 1u) / 256u - blk0 + 1u;
+        memset(stats, 0, (size_t)nblk * 4u * sizeof(uint32_t));
+    }
+    for (uint32_t k = 0; k < K; ++k) {
+        uint32_t t = sim->t + k;
+        for (uint32_t i = 0; i < n; ++i) {
+            uint32_t env = sim->env0 + i;
+            float cur[4], nxt[4];
+            for (int c = 0; c < 4; ++c) cur[c] = sim->cart[(size_t)c * n + i];
+
+            int a;
+            if (pol) {
+                double p0 = orc_mlp_p0(pol, cur);
+                float u = orc_policy_u(sim->seed, env, t);
+                a = ((double)u < p0) ? 0 : 1;
+                if (p0_out) p0_out[(size_t)k * n + i] = p0;
+            } else {
+                a = orc_action_bit(sim->seed, env, t);
+            }
+
+            orc_cartpole_step(&sim->p, cur, a, nxt);
+            for (uint32_t j = 0; j < sim->D; ++j) {
+                size_t q = (size_t)j * n + i;
+                sim->s[q] = orc_pad_update(sim->s[q], sim->a[q], sim->b[q], a);
+            }
+
+            uint32_t len = sim->ep[i] + 1u;
+            int term = orc_terminated(&sim->p, nxt);
+            int trunc = (sim->p.max_episode_steps != 0u) && (len >= sim->p.max_episode_steps);
+            uint8_t d = (uint8_t)(term | (trunc << 1));
+
+            if (obs) for (int c = 0; c < 4; ++c) obs[((size_t)k * 4 + c) * n + i] = cur[c];
+            if (act) act[(size_t)k * n + i] = (uint8_t)a;
+            if (rew) rew[(size_t)k * n + i] = 1.0f;
+            if (done) done[(size_t)k * n + i] = d;
+
+            if (d) {
+                orc_reset_draw(&sim->p, sim->seed, env, t + 1u, nxt);
+                sim->ep[i] = 0;
+                for (uint32_t j = 0; j < sim->D; ++j) sim->s[(size_t)j * n + i] = 0.0f;
+                if (stats) {
+                    uint32_t* st = stats + (size_t)(env / 256u - blk0) * 4u;
+                    st[0] += 1u;
+                    st[1] += len;
+                    st[2] += (uint32_t)term;
+                    st[3] += (uint32_t)trunc;
+                }
+            } else {
+                sim->ep[i] = len;
+            }
+            for (int c = 0; c < 4; ++c) sim->cart[(size_t)c * n + i] = nxt[c];
+        }
+    }
+    sim->t += K;
+    return 0;
+}
+
+/* State as [4 + D][n] words (cart-pole words, then padding), episode steps,
+ * and the global step counter. */
+void orc_get_state(const orc_sim* sim, float* state, uint32_t* ep, uint64_t* t)
+{
+    size_t n = sim->n;
+    if (state) {
+        memcpy(state, sim->cart, 4 * n * sizeof(float));
+        if (sim->D) memcpy(state + 4 * n, sim->s, (size_t)sim->D * n * sizeof(float));
+    }
+    if (ep) memcpy(ep, sim->ep, n * sizeof(uint32_t));
+    if (t) *t = sim->t;
+}
+
+/* Overwrite the state; the padding parameters stay those of the last reset. */
+int orc_set_state(orc_sim* sim, const float* state, const uint32_t* ep, uint64_t t)
+{
+    if (!sim->has_reset) return -1;
+    if (t > 0xFFFFFFFFull) return -2;
+    size_t n = sim->n;
+    if (state) {
+        memcpy(sim->cart, state, 4 * n * sizeof(float));
+        if (sim->D) memcpy(sim->s, state + 4 * n, (size_t)sim->D * n * sizeof(float));
+    }
+    if (ep) memcpy(sim->ep, ep, n * sizeof(uint32_t));
+    sim->t = (uint32_t)t;
+    return 0;
+}
+
+/* Padding parameters as [D][n] arrays (for tests of the recurrence). */
+void orc_get_pad_params(const orc_sim* sim, float* a, float* b)
+{
+    size_t nd = (size_t)sim->D * sim->n;
+    if (a && nd) memcpy(a, sim->a, nd * sizeof(float));
+    if (b && nd) memcpy(b, sim->b, nd * sizeof(float));
+}

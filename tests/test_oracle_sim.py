@@ -1,0 +1,247 @@
+"""Pins of the oracle's vectorised data-collection loop (CPU only).
+
+Invariants and closed forms the loop must satisfy whatever its internals:
+
+* every trajectory row continues the previous one: the next obs is the Euler
+  step of (obs, action), or, after done, the reset draw of the next step;
+* done bit 0 <=> the post-step state crossed a threshold; bit 1 <=> the
+  episode reached the time limit; stored episode counters stay below it;
+* results do not depend on how K steps are split into calls, or on which
+  slice of environments is simulated (counter-based RNG keyed by global id);
+* the padding words follow the closed form of their linear recurrence;
+* block statistics equal a brute-force recount from the trajectory;
+* random-action episode lengths have the cart-pole's known scale.
+"""
+import math
+from fractions import Fraction
+
+import mpmath
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+P = oracle.make_params(**workloads.CARTPOLE)
+
+
+def _run(n, T, K, D=0, seed=0, env0=0, params=P, policy=None):
+    sim = oracle.Sim(n, D, params, env0=env0)
+    sim.reset(seed)
+    parts = []
+    done_steps = 0
+    while done_steps < T:
+        k = min(K, T - done_steps)
+        parts.append(sim.step(k, policy=policy))
+        done_steps += k
+    traj = {key: np.concatenate([p[key] for p in parts], axis=0) for key in ("obs", "action", "reward", "done")}
+    traj["stats"] = [p["stats"] for p in parts]
+    return sim, traj
+
+
+def test_reset_state_in_box_and_counters_zero():
+    sim = oracle.Sim(1000, 3, P)
+    sim.reset(5)
+    st, ep, t = sim.get_state()
+    assert t == 0 and np.all(ep == 0)
+    assert np.all(st[:4] >= np.float32(-0.05)) and np.all(st[:4] <= np.float32(0.05))
+    assert np.all(st[4:] == 0) and not np.any(np.signbit(st[4:]))
+    a, b = sim.pad_params()
+    assert np.all(a >= np.float32(0.9)) and np.all(a <= np.float32(0.99))
+    assert np.all(b >= np.float32(-1)) and np.all(b <= np.float32(1))
+
+
+def test_trajectory_rows_chain_and_done_semantics():
+    n, T = 64, 300
+    sim, tr = _run(n, T, K=T, seed=1)
+    obs, act, rew, done = tr["obs"], tr["action"], tr["reward"], tr["done"]
+    assert np.all(rew == 1.0)
+    assert set(np.unique(act)) <= {0, 1}
+    assert set(np.unique(done)) <= {0, 1, 2, 3}
+    final, _, t = sim.get_state()
+    assert t == T
+    for e in range(n):
+        for t in range(T):
+            post = oracle.cartpole_step(P, obs[t, :, e], int(act[t, e]))
+            term = oracle.terminated(P, post)
+            assert (done[t, e] & 1) == int(term)
+            nxt = obs[t + 1, :, e] if t + 1 < T else final[:4, e]
+            if done[t, e]:
+                assert np.array_equal(nxt, oracle.reset_draw(P, 1, e, t + 1))
+            else:
+                assert np.array_equal(nxt, post)
+            assert act[t, e] == oracle.action_bit(1, e, t)
+
+
+def test_time_limit_and_counters():
+    params = oracle.make_params(**workloads.cartpole(max_episode_steps=5, x_threshold=1e9, theta_threshold_rad=1e9))
+    sim, tr = _run(8, 23, K=23, params=params)
+    done = tr["done"]
+    # only truncations, every 5th step
+    expect = np.zeros(23, dtype=np.uint8)
+    expect[4::5] = 2
+    assert np.array_equal(done, np.repeat(expect[:, None], 8, axis=1))
+    _, ep, _ = sim.get_state()
+    assert np.all(ep == 23 % 5)
+    # default limit: no run of more than 500 steps without done, counters < 500
+    params = oracle.make_params(**workloads.cartpole(no_termination=1))
+    sim, tr = _run(2, 1200, K=600, params=params)
+    d = tr["done"]
+    assert np.array_equal(np.nonzero(d[:, 0])[0], np.array([499, 999]))
+    assert np.all(d[[499, 999]] == 2)
+    _, ep, _ = sim.get_state()
+    assert np.all(ep < 500)
+
+
+def test_terminated_and_truncated_together():
+    # a threshold that is crossed exactly on the 3rd step of every episode
+    params = oracle.make_params(**workloads.cartpole(max_episode_steps=3, x_threshold=1e9, theta_threshold_rad=1e9))
+    _, tr = _run(4, 9, K=9, params=params)
+    assert np.all(tr["done"][2::3] == 2)
+    tight = oracle.make_params(**workloads.cartpole(max_episode_steps=1, theta_threshold_rad=0.0))
+    _, tr = _run(4, 4, K=4, params=tight)
+    # every step terminates (any nonzero angle) and is truncated (limit 1), unless theta' == 0 exactly
+    assert np.all(tr["done"] == 3)
+
+
+@pytest.mark.parametrize("D", [0, 5])
+def test_partition_invariance(D):
+    n, T = 37, 130
+    base_sim, base = _run(n, T, K=T, D=D, seed=3)
+    for K in (1, 7, 64):
+        sim, tr = _run(n, T, K=K, D=D, seed=3)
+        for key in ("obs", "action", "reward", "done"):
+            assert np.array_equal(tr[key], base[key]), (K, key)
+        s1, e1, t1 = sim.get_state()
+        s0, e0, t0 = base_sim.get_state()
+        assert np.array_equal(s1, s0) and np.array_equal(e1, e0) and t1 == t0
+
+
+def test_slice_invariance():
+    # env e behaves the same whether simulated alone or inside a larger batch
+    n, T = 300, 80
+    _, full = _run(n, T, K=40, D=2, seed=workloads.PARITY_SEEDS[2])
+    for e in (0, 17, 255, 256, 299):
+        _, one = _run(1, T, K=T, D=2, seed=workloads.PARITY_SEEDS[2], env0=e)
+        for key in ("obs", "action", "done"):
+            assert np.array_equal(one[key][..., 0], full[key][..., e]), (e, key)
+
+
+def test_get_set_state_resume():
+    n, T = 50, 120
+    _, whole = _run(n, T, K=T, D=3, seed=9)
+    sim = oracle.Sim(n, 3, P)
+    sim.reset(9)
+    first = sim.step(T // 2)
+    st, ep, t = sim.get_state()
+    sim2 = oracle.Sim(n, 3, P)
+    sim2.reset(9)                      # same padding parameters
+    sim2.set_state(st, ep, t)
+    second = sim2.step(T - T // 2)
+    for key in ("obs", "action", "done"):
+        assert np.array_equal(np.concatenate([first[key], second[key]]), whole[key])
+
+
+def test_step_before_reset_and_overflow():
+    sim = oracle.Sim(4, 0, P)
+    with pytest.raises(RuntimeError):
+        sim.step(1)
+    sim.reset(0)
+    st, ep, _ = sim.get_state()
+    sim.set_state(st, ep, 2**32 - 10)
+    sim.step(9)
+    with pytest.raises(RuntimeError):
+        sim.step(2)
+
+
+def test_block_stats_brute_force():
+    n, T = 700, 150
+    env0 = 200      # a slice straddling block boundaries
+    sim = oracle.Sim(n, 0, P, env0=env0)
+    sim.reset(2)
+    pre = sim.step(37)                  # stats are per call
+    _, ep_start, _ = sim.get_state()
+    out = sim.step(T)
+    done = out["done"]
+    nblk = sim.n_blocks
+    want = np.zeros((nblk, 4), dtype=np.int64)
+    for i in range(n):
+        blk = (env0 + i) // 256 - env0 // 256
+        length = int(ep_start[i])
+        for t in range(T):
+            length += 1
+            if done[t, i]:
+                want[blk] += [1, length, done[t, i] & 1, (done[t, i] >> 1) & 1]
+                length = 0
+    assert np.array_equal(out["stats"].astype(np.int64), want)
+    assert want[:, 0].sum() > 0 and pre["stats"].sum() > 0
+
+
+def test_episode_length_scale():
+    """Random pushes topple the pole in about 22 steps on average (at least 8)."""
+    n, T = 2000, 400
+    _, tr = _run(n, T, K=T, seed=0)
+    d = tr["done"]
+    lengths = []
+    for e in range(n):
+        idx = np.nonzero(d[:, e])[0]
+        lengths.extend(np.diff(np.concatenate([[-1], idx])).tolist())
+    lengths = np.array(lengths)
+    assert 20.0 < lengths.mean() < 25.0
+    assert lengths.min() >= 8
+    assert np.all(d & 2 == 0)        # no episode reaches 500 steps here
+
+
+def _forced_action_policy(action):
+    """Zero weights and output biases that put all mass on one action."""
+    z = lambda *s: np.zeros(s, dtype=np.float32)  # noqa: E731
+    b3 = np.array([50.0, -50.0] if action == 0 else [-50.0, 50.0], dtype=np.float32)
+    return oracle.Policy(z(64, 4), z(64), z(64, 64), z(64), z(2, 64), b3)
+
+
+def test_padding_closed_form_constant_action():
+    """With a_t = 1 throughout an episode, s_n = b (1 - a^n) / (1 - a); fp32
+    rounding adds at most ~n ulp-sized errors, bounded by n eps |b| / (1 - a).
+    Gravity and force are off so that the cart-pole stays finite without
+    termination (a NaN observation would make the policy's p0 NaN)."""
+    params = oracle.make_params(**workloads.cartpole(no_termination=1, max_episode_steps=0,
+                                                     gravity=0.0, force_mag=0.0))
+    D, n, T = 6, 8, 60
+    sim = oracle.Sim(n, D, params)
+    sim.reset(4)
+    a, b = sim.pad_params()
+    sim.step(T, policy=_forced_action_policy(1))
+    st, _, _ = sim.get_state()
+    for j in range(D):
+        for e in range(n):
+            aa, bb = Fraction(float(a[j, e])), Fraction(float(b[j, e]))
+            exact = bb * (1 - aa**T) / (1 - aa)
+            bound = T * 2.0**-24 * abs(float(bb)) / (1 - float(aa))
+            assert abs(float(st[4 + j, e]) - float(exact)) <= bound
+    # action 0 throughout: the words stay exactly +0
+    sim.reset(4)
+    sim.step(T, policy=_forced_action_policy(0))
+    st, _, _ = sim.get_state()
+    assert np.all(st[4:] == 0) and not np.any(np.signbit(st[4:]))
+
+
+def test_padding_closed_form_random_actions():
+    """Within an episode that starts at t0, s_t = sum_{i<t} a^(t-1-i) b u_i."""
+    D, n, T = 3, 16, 90
+    sim = oracle.Sim(n, D, P)
+    sim.reset(6)
+    a, b = sim.pad_params()
+    tr = sim.step(T)
+    st, _, _ = sim.get_state()
+    act, done = tr["action"], tr["done"]
+    with mpmath.workdps(40):
+        for e in range(n):
+            last_done = np.nonzero(done[:, e])[0]
+            t0 = int(last_done[-1]) + 1 if len(last_done) else 0
+            for j in range(D):
+                aa, bb = mpmath.mpf(float(a[j, e])), mpmath.mpf(float(b[j, e]))
+                exact = mpmath.fsum(aa ** (T - 1 - i) * bb * int(act[i, e]) for i in range(t0, T))
+                bound = (T - t0) * 2.0**-24 * abs(float(bb)) / (1 - float(aa)) + 1e-30
+                assert abs(float(st[4 + j, e]) - float(exact)) <= bound, (e, j)
+                if t0 == T:
+                    assert st[4 + j, e] == 0
