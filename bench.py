@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused data-collection kernel on one MI355X.
+
+One bench "step" is one pass of the whole hot path over the headline workload:
+4,194,304 cart-pole environments advanced 200 steps by ONE launch of the fused
+kernel (K = 200), writing the full trajectory (obs f32 x 4, action u8, reward
+f32, done u8 per env-step) and the per-256-env block statistics.  Inputs are
+synthetic: the library draws every initial state and action on the device from
+Philox keyed by the seed.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--no-cpu] [--no-unfused]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+METRIC = "env-steps/sec at 1 MI355X; achieved HBM GB/s vs peak; fused/unfused speedup"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_source_digest() -> str:
+    """Digest of the kernel sources: a stored traffic measurement is used only
+    while the kernels it was taken on are unchanged."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2207_07736_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = d.get(workload)
+    if not e or e.get("source_digest") != kernel_source_digest():
+        return None
+    return float(e["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
+    """The oracle (single-threaded C loop, as it stands) on a bounded sample of
+    the headline workload: `slices` env slices of the 4M batch, T steps each."""
+    import oracle
+    params = oracle.make_params(**workloads.CARTPOLE)
+    n_total = workloads.WORKLOADS["C3"]["n"]
+    stride = n_total // slices
+    elapsed = 0.0
+    for i in range(slices):
+        sim = oracle.Sim(n_slice_envs, 0, params, env0=i * stride)
+        sim.reset(seed)
+        t0 = time.perf_counter()
+        sim.step(T)
+        elapsed += time.perf_counter() - t0
+        del sim
+    env_steps = n_slice_envs * slices * T
+    return {"value": env_steps / elapsed, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps of the 4,194,304-env headline batch "
+                      f"(seed {seed}, trajectory recorded), {elapsed:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-unfused", action="store_true", help="skip the K=1 contrast")
+    ap.add_argument("--cpu-slice-envs", type=int, default=65536)
+    ap.add_argument("--cpu-slices", type=int, default=8)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the environments shard by range with no "
+              "communication, so a multi-GPU figure is N times the one-GPU figure and is not measured here.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    w = workloads.WORKLOADS["C3"]
+    n, T, K = w["n"], w["T"], w["K"][0]
+    seed = w["seed"]
+    stream = torch.cuda.current_stream()
+
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(seed)
+    traj = Trajectory(T, n)
+    rows = traj.rows(0, K)
+    print(f"[bench] workload {w['name']}: n={n} T={T} K={K} warmup={args.warmup} steps={args.steps}",
+          file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        sim.step(K, rows)
+    torch.cuda.synchronize()
+
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        sim.step(K, rows)           # exactly one kernel launch
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
+    env_steps_per_s = n * T / (ms_per_step * 1e-3)
+
+    # Algorithmic bytes per launch: the trajectory (22 B per env-step), the
+    # state read and written once (4 x f32 + u32 episode counter, each way) and
+    # 16 B of block statistics per 256 envs.
+    algo_bytes = n * T * workloads.TRAJ_BYTES_PER_ENV_STEP + n * 2 * 20 + (n // 256) * 16
+    achieved_gbs = algo_bytes / (ms_per_step * 1e-3) / 1e9
+    traffic = stored_traffic(w["name"])
+
+    result = {
+        "metric": METRIC,
+        "value": env_steps_per_s,
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (device Philox draws from seed 0)",
+        "config": {"workload": w["name"], "n_envs": n, "steps_per_run": T, "steps_per_launch": K,
+                   "padding_words": 0, "policy": "random", "trajectory": "obs f32x4, action u8, reward f32, done u8"},
+        "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_cartpole_fused<0,REC,STATS>", "algorithmic_bytes_per_launch": algo_bytes},
+        "wall_s_timed_region": wall,
+    }
+
+    if not args.no_unfused:
+        # the same 200 steps as 200 launches of K = 1 (state to and from HBM every step)
+        sim.reset(seed)
+        row_structs = [traj.rows(k, 1) for k in range(T)]      # marshalled before timing
+        for k in range(T):
+            sim.step(1, row_structs[k])
+        torch.cuda.synchronize()
+        reps = 3
+        start.record(stream)
+        for _ in range(reps):
+            for k in range(T):
+                sim.step(1, row_structs[k])
+        stop.record(stream)
+        torch.cuda.synchronize()
+        unfused_ms = start.elapsed_time(stop) / reps
+        result["fusion"] = {"unfused_K1_ms": unfused_ms, "fused_K200_ms": ms_per_step,
+                            "speedup": unfused_ms / ms_per_step,
+                            "unfused_algorithmic_GBs": (n * T * (workloads.TRAJ_BYTES_PER_ENV_STEP + 40)) / (unfused_ms * 1e-3) / 1e9}
+
+    del traj
+    sim.close()
+
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(args.cpu_slice_envs, args.cpu_slices, T, seed)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,161 @@
+/*
+ * rlsim.h -- C ABI of the GPU-vectorised, kernel-fused cart-pole data collector.
+ *
+ * The operation is the data-collection loop of Gleeson et al., "Optimizing Data
+ * Collection in Deep Reinforcement Learning" (2022): N simulator instances are
+ * stepped together on the GPU (section "GPU Vectorization"), K consecutive
+ * simulation steps run inside one kernel launch with the simulator state held
+ * in registers (section "Simulator Kernel Fusion"), and each step feeds the
+ * state to a policy whose action drives the next state and reward (Background,
+ * "RL Training" and the data-collection figure).  The simulator is cart-pole
+ * (Background, "Cartpole Simulator"), optionally widened by D extra state words
+ * per environment (the state-size factor S of "Simulator Complexity").
+ *
+ * Conventions for every call:
+ *  - Returns RLSIM_OK (0) or a negative rlsim_status; rlsim_last_error() gives
+ *    the message.  No exception crosses the ABI.
+ *  - A handle is not thread-safe.  The library owns the simulator state (device
+ *    memory it allocates in rlsim_create and frees in rlsim_destroy); the caller
+ *    owns every buffer it passes in and the library never frees or keeps them.
+ *  - Work is enqueued asynchronously on the handle's HIP stream (cfg.stream);
+ *    only rlsim_get_state, rlsim_set_state and rlsim_destroy synchronise it.
+ *    A kernel fault surfaces as RLSIM_EDEVICE at a later call.
+ *  - "Device pointer" means memory the current HIP device can access (hipMalloc,
+ *    torch tensors on that device).  Host pointers are plain process memory.
+ */
+#ifndef RLSIM_H
+#define RLSIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RLSIM_OK = 0,
+    RLSIM_EINVAL = -1,       /* bad argument: sizes, NULLs, alignment, ranges */
+    RLSIM_ENOMEM = -2,       /* device allocation failed */
+    RLSIM_EDEVICE = -3,      /* a HIP runtime call failed (message has its text) */
+    RLSIM_ESTATE = -4,       /* call not valid in the handle's state (step before reset) */
+    RLSIM_EUNSUPPORTED = -5  /* valid request this build does not implement */
+} rlsim_status;
+
+enum { RLSIM_F32 = 0, RLSIM_BF16 = 1 };       /* rlsim_policy.dtype */
+enum { RLSIM_F_NO_TERMINATION = 1u };         /* rlsim_cfg.flags: thresholds never fire */
+
+typedef struct rlsim rlsim_t;                 /* opaque handle */
+
+/* Simulator constants (fp32; the paper cites cart-pole but prints none) and the
+ * stream the handle enqueues on.  rlsim_cfg_default fills the classic values:
+ * g = 9.8, cart 1.0, pole 0.1, half length 0.5, force 10, tau 0.02, |x| limit
+ * 2.4, |theta| limit = fp32(12 * 2 pi / 360), 500-step episodes, reset box
+ * [-0.05, 0.05), padding a in [0.9, 0.99), b in [-1, 1), flags 0, stream NULL. */
+typedef struct {
+    float gravity, masscart, masspole, half_length, force_mag, tau;
+    float x_threshold, theta_threshold_rad;
+    uint32_t max_episode_steps;            /* 0 = no time limit */
+    float reset_low, reset_high;           /* initial-state box, each word */
+    float pad_a_low, pad_a_high;           /* padding decay a_j */
+    float pad_b_low, pad_b_high;           /* padding gain b_j */
+    uint32_t flags;                        /* RLSIM_F_* */
+    void* stream;                          /* hipStream_t; NULL = default stream */
+} rlsim_cfg;
+
+/* Fill *cfg with the defaults above.  NULL cfg: no effect. */
+void rlsim_cfg_default(rlsim_cfg* cfg);
+
+/* Create a simulator of n_envs environments with state_words = 4 + D fp32 words
+ * each (4 cart-pole words x, x_dot, theta, theta_dot, then D padding words),
+ * on the current HIP device.  Allocates the state (about (20 + 12 D) bytes per
+ * environment) on the device.  cfg may be NULL (defaults).
+ * Errors: EINVAL if out == NULL, n_envs == 0 or n_envs > 2^30, state_words < 4,
+ * a non-finite or inconsistent constant (masses <= 0, half_length <= 0,
+ * reset_low > reset_high, ...); ENOMEM; EDEVICE.  On error *out is NULL. */
+int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rlsim_t** out);
+
+/* Start every environment's first episode at global step t = 0 (Background,
+ * "RL Training": the loop's initial simulator state).  The state is drawn from
+ * Philox4x32-10 keyed by seed (stream RESET), the episode counters are zeroed,
+ * the padding words set to +0 and their parameters a_j, b_j drawn (stream
+ * PARAMS).  Enqueues one kernel per state array; does not synchronise.
+ * Errors: EINVAL (h NULL), EDEVICE. */
+int rlsim_reset(rlsim_t* h, uint64_t seed);
+
+/* Caller-owned DEVICE buffers receiving rows 0..K-1 of one rlsim_step_fused
+ * call; row k holds global step t + k.  Layout is structure-of-arrays so that
+ * consecutive environments are consecutive addresses:
+ *   obs        [K][4][n_envs] f32  state before the step (x, x_dot, th, th_dot)
+ *   action     [K][n_envs]    u8   0 = push towards -x, 1 = towards +x
+ *   reward     [K][n_envs]    f32  1.0 every step
+ *   done       [K][n_envs]    u8   bit 0 terminated, bit 1 time limit reached
+ *   block_stats[ceil(n_envs/256)][4] u32, optional, overwritten each call:
+ *              per 256-environment block {episodes finished, sum of their
+ *              lengths, terminated, truncated} over this call's K steps
+ *   policy_p0  [K][n_envs]    f32  optional; policy runs only: the policy's
+ *              probability of action 0 at each step
+ * obs, action, reward and done are all set or all NULL (no trajectory). */
+typedef struct {
+    float* obs;
+    uint8_t* action;
+    float* reward;
+    uint8_t* done;
+    uint32_t* block_stats;
+    float* policy_p0;
+} rlsim_traj;
+
+/* Caller-owned DEVICE weights of the MLP policy 4 -> 64 -> 64 -> 2 (tanh hidden
+ * layers; the inference half of the simulation/inference loop, fused with the
+ * simulator as the paper's Future Work proposes).  Weights are row-major
+ * [out][in] in dtype (RLSIM_F32: float, RLSIM_BF16: bfloat16 bits as uint16);
+ * biases are always float and may be NULL (zero). */
+typedef struct {
+    int dtype;
+    const void* w1; const float* b1;    /* 64 x 4,  64 */
+    const void* w2; const float* b2;    /* 64 x 64, 64 */
+    const void* w3; const float* b3;    /* 2 x 64,  2  */
+} rlsim_policy;
+
+/* Run global steps t .. t+K-1 of every environment in exactly one kernel launch
+ * (the paper's fused simulation, "Simulator Kernel Fusion"), then t += K.  K = 1
+ * is the unfused form: the state goes to and from device memory every step.
+ * Each step: record obs; choose the action (random Philox bit, or sample the
+ * policy: action 0 with probability p0 = softmax(logits)[0]); Euler-step the
+ * cart-pole; update padding words s_j <- a_j s_j + b_j * action (one rounding);
+ * terminated = |x| > x_threshold or |theta| > theta_threshold (strict), truncated
+ * = episode length reached max_episode_steps; reward 1; after done the next
+ * episode starts from the reset draw of step t+k+1 with zero padding words.
+ * policy_or_null: NULL = random actions.  traj_or_null: NULL = record nothing.
+ * Errors: EINVAL (h NULL, K == 0, t + K > 2^32 - 1, a mixed set of NULL
+ * trajectory pointers, a float pointer not 4-byte aligned, policy_p0 without a
+ * policy, a policy with NULL weights or unknown dtype); ESTATE (before
+ * rlsim_reset); EUNSUPPORTED (a policy with D > 0); EDEVICE. */
+int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy_or_null,
+                     const rlsim_traj* traj_or_null);
+
+/* Copy the state to HOST memory and synchronise the stream.  host_state:
+ * [state_words][n_envs] f32 (cart-pole words then padding words), host_ep:
+ * [n_envs] u32 steps taken in the current episode, *t_out: next global step.
+ * Any pointer may be NULL (skipped).  Errors: EINVAL, ESTATE, EDEVICE. */
+int rlsim_get_state(rlsim_t* h, float* host_state, uint32_t* host_ep, uint64_t* t_out);
+
+/* Overwrite the state from HOST memory (same layouts) and set the global step
+ * to t (checkpoint resume; padding parameters stay those of the last reset).
+ * NULL host_state / host_ep leave that part unchanged.  Synchronises.
+ * Errors: EINVAL (t > 2^32 - 1), ESTATE (before reset), EDEVICE. */
+int rlsim_set_state(rlsim_t* h, const float* host_state, const uint32_t* host_ep, uint64_t t);
+
+/* Synchronise the stream and free the handle and its device memory.  NULL is
+ * accepted (returns RLSIM_OK). */
+int rlsim_destroy(rlsim_t* h);
+
+/* Message of h's last failure ("" if none).  h == NULL: the calling thread's
+ * last rlsim_create failure.  The string stays valid until the next call on h
+ * (or the thread's next create). */
+const char* rlsim_last_error(const rlsim_t* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RLSIM_H */

@@ -1,0 +1,135 @@
+// device_common.hip.h -- RNG, uniform mapping and the cart-pole step, as gfx950
+// device functions used by every simulator kernel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rlsim_dev {
+
+// ---------------------------------------------------------------------------
+// Kernel-side constants.  Computed once on the host from rlsim_cfg, each by one
+// fp32 operation (see make_dev_params in rlsim.hip).
+// ---------------------------------------------------------------------------
+struct DevParams {
+    float gravity, force_mag, tau, half_length;
+    float pole_ml;        // masspole * half_length
+    float inv_total;      // 1 / (masscart + masspole)
+    float m_over_M;       // masspole * inv_total
+    float ml_over_M;      // pole_ml * inv_total
+    float four_thirds;    // 4 / 3
+    float thr_x, thr_th;  // +inf when termination is disabled
+    uint32_t max_steps;   // 0 = no time limit
+    float reset_lo, reset_width;   // width = reset_high - reset_low
+    uint32_t key0, key1;  // Philox key: low and high word of the seed
+};
+
+// Counter stream ids (third counter word).
+enum : uint32_t { STREAM_RESET = 0u, STREAM_ACTION = 1u, STREAM_PARAMS = 2u, STREAM_POLICY = 3u };
+
+// Philox4x32-10 (Salmon et al., SC'11) on counter (c0, c1, c2, 0) and key
+// (k0, k1).  c1, c2 and the key are wave-uniform in every caller, so the first
+// round's second product and the whole key schedule land on the scalar unit.
+__device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t k0, uint32_t k1)
+{
+    uint32_t c3 = 0u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo0 = 0xD2511F53u * c0;
+        const uint32_t hi0 = __umulhi(0xD2511F53u, c0);
+        const uint32_t lo1 = 0xCD9E8D57u * c2;
+        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2);
+        const uint32_t n0 = hi1 ^ c1 ^ k0;
+        const uint32_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return make_uint4(c0, c1, c2, c3);
+}
+
+// Top 24 bits of r as a float in [0, 1 - 2^-24] (exact), then lo + u * width
+// with a single rounding.
+__device__ __forceinline__ float u24(uint32_t r) { return (float)(r >> 8) * 0x1.0p-24f; }
+__device__ __forceinline__ float uniform01_to(uint32_t r, float lo, float width)
+{
+    return __builtin_fmaf(u24(r), width, lo);
+}
+
+// Series sin / cos of degree 9 / 8, Horner form, one rounding per operation.
+// Accurate to < 1 ulp for |th| <= 12 degrees (every pre-step angle of a live
+// episode).
+__device__ __forceinline__ void sincos_series(float th, float& s, float& c)
+{
+    const float s3 = (float)(-1.0 / 6.0), s5 = (float)(1.0 / 120.0);
+    const float s7 = (float)(-1.0 / 5040.0), s9 = (float)(1.0 / 362880.0);
+    const float c2 = -0.5f, c4 = (float)(1.0 / 24.0);
+    const float c6 = (float)(-1.0 / 720.0), c8 = (float)(1.0 / 40320.0);
+    const float z = th * th;
+    float qs = __builtin_fmaf(s9, z, s7);
+    qs = __builtin_fmaf(qs, z, s5);
+    qs = __builtin_fmaf(qs, z, s3);
+    s = __builtin_fmaf(th * z, qs, th);
+    float qc = __builtin_fmaf(c8, z, c6);
+    qc = __builtin_fmaf(qc, z, c4);
+    qc = __builtin_fmaf(qc, z, c2);
+    c = __builtin_fmaf(z, qc, 1.0f);
+}
+
+// One explicit-Euler step of the frictionless cart with a uniform rod:
+//   thacc = (g sin - cos * temp) / (l (4/3 - m cos^2 / M)),
+//   temp  = (F + m l thd^2 sin) / M,   xacc = temp - (m l / M) thacc cos,
+// positions advanced with the old velocities.  act 1 pushes towards +x.
+struct CartState { float x, xd, th, thd; };
+
+__device__ __forceinline__ CartState cartpole_step(const DevParams& p, const CartState& s, uint32_t act)
+{
+    const float force = act ? p.force_mag : -p.force_mag;
+    float sn, cs;
+    sincos_series(s.th, sn, cs);
+    const float ml_thd2 = p.pole_ml * (s.thd * s.thd);
+    const float temp = __builtin_fmaf(ml_thd2, sn, force) * p.inv_total;
+    const float num = __builtin_fmaf(-cs, temp, p.gravity * sn);
+    const float den = p.half_length * __builtin_fmaf(-p.m_over_M, cs * cs, p.four_thirds);
+    const float thacc = num / den;                       // IEEE division
+    const float xacc = __builtin_fmaf(-(p.ml_over_M * thacc), cs, temp);
+    CartState o;
+    o.x = __builtin_fmaf(p.tau, s.xd, s.x);
+    o.xd = __builtin_fmaf(p.tau, xacc, s.xd);
+    o.th = __builtin_fmaf(p.tau, s.thd, s.th);
+    o.thd = __builtin_fmaf(p.tau, thacc, s.thd);
+    return o;
+}
+
+// Strict thresholds; NaN compares false.  Disabled termination is encoded as
+// infinite thresholds, under which every comparison is false.
+__device__ __forceinline__ uint32_t crossed(const DevParams& p, const CartState& s)
+{
+    return (uint32_t)((s.x < -p.thr_x) | (s.x > p.thr_x) | (s.th < -p.thr_th) | (s.th > p.thr_th));
+}
+
+// Byte offset addressing: base + 32-bit unsigned offset lets the compiler use a
+// scalar base register plus a per-lane 32-bit offset (n_envs <= 2^30).
+template <class T>
+__device__ __forceinline__ T* at(T* base, uint32_t byte_off)
+{
+    return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + byte_off);
+}
+template <class T>
+__device__ __forceinline__ const T* at(const T* base, uint32_t byte_off)
+{
+    return reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
+// Sum over the 64 lanes of a wave (every lane gets the total).
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off, 64);
+    return v;
+}
+
+}  // namespace rlsim_dev

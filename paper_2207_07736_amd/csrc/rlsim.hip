@@ -1,0 +1,351 @@
+// rlsim.hip -- host runtime of the C ABI declared in include/rlsim.h:
+// argument checks, device state ownership, kernel selection and launch.
+#include "rlsim.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "k_cartpole.hip.h"
+
+using namespace rlsim_dev;
+
+struct rlsim {
+    uint32_t n = 0;             // environments
+    uint32_t D = 0;             // padding words per environment
+    int device = 0;
+    hipStream_t stream = nullptr;
+    rlsim_cfg cfg{};
+    DevParams dp{};
+    uint64_t t = 0;             // global step of the next step
+    bool has_reset = false;
+    float* cart = nullptr;      // [4][n]
+    uint32_t* ep = nullptr;     // [n]
+    float* pad_s = nullptr;     // [D][n]
+    float* pad_a = nullptr;
+    float* pad_b = nullptr;
+    std::string err;
+};
+
+namespace {
+
+thread_local std::string g_create_err;
+
+int fail(rlsim* h, int code, const std::string& msg)
+{
+    if (h) h->err = msg;
+    else g_create_err = msg;
+    return code;
+}
+
+int hip_fail(rlsim* h, hipError_t e, const char* what)
+{
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    return fail(h, RLSIM_EDEVICE, m);
+}
+
+// Makes the handle's device current for the scope, restoring the caller's.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+        if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+    }
+    ~DeviceGuard()
+    {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+bool finite(float v) { return std::isfinite(v); }
+
+// Kernel constants, each one fp32 operation on the configured values.
+DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
+{
+    DevParams p{};
+    volatile float total = c.masscart + c.masspole;    // volatile: one rounding per line
+    volatile float pole_ml = c.masspole * c.half_length;
+    volatile float inv_total = 1.0f / total;
+    volatile float m_over_M = c.masspole * inv_total;
+    volatile float ml_over_M = pole_ml * inv_total;
+    volatile float four_thirds = 4.0f / 3.0f;
+    volatile float width = c.reset_high - c.reset_low;
+    p.gravity = c.gravity;
+    p.force_mag = c.force_mag;
+    p.tau = c.tau;
+    p.half_length = c.half_length;
+    p.pole_ml = pole_ml;
+    p.inv_total = inv_total;
+    p.m_over_M = m_over_M;
+    p.ml_over_M = ml_over_M;
+    p.four_thirds = four_thirds;
+    const bool noterm = (c.flags & RLSIM_F_NO_TERMINATION) != 0u;
+    p.thr_x = noterm ? INFINITY : c.x_threshold;
+    p.thr_th = noterm ? INFINITY : c.theta_threshold_rad;
+    p.max_steps = c.max_episode_steps;
+    p.reset_lo = c.reset_low;
+    p.reset_width = width;
+    p.key0 = (uint32_t)(seed & 0xFFFFFFFFull);
+    p.key1 = (uint32_t)(seed >> 32);
+    return p;
+}
+
+const char* check_cfg(const rlsim_cfg& c)
+{
+    const float vals[] = {c.gravity, c.masscart, c.masspole, c.half_length, c.force_mag, c.tau, c.x_threshold,
+                          c.theta_threshold_rad, c.reset_low, c.reset_high, c.pad_a_low, c.pad_a_high,
+                          c.pad_b_low, c.pad_b_high};
+    for (float v : vals)
+        if (!finite(v)) return "cfg: every constant must be finite";
+    if (!(c.masscart > 0.0f) || !(c.masspole > 0.0f)) return "cfg: masses must be positive";
+    if (!(c.half_length > 0.0f)) return "cfg: half_length must be positive";
+    if (!(c.tau > 0.0f)) return "cfg: tau must be positive";
+    if (c.reset_low > c.reset_high) return "cfg: reset_low > reset_high";
+    if (c.pad_a_low > c.pad_a_high || c.pad_b_low > c.pad_b_high) return "cfg: padding range low > high";
+    if ((c.flags & ~(uint32_t)RLSIM_F_NO_TERMINATION) != 0u) return "cfg: unknown flag bits";
+    return nullptr;
+}
+
+void free_state(rlsim* h)
+{
+    if (h->cart) (void)hipFree(h->cart);
+    if (h->ep) (void)hipFree(h->ep);
+    if (h->pad_s) (void)hipFree(h->pad_s);
+    if (h->pad_a) (void)hipFree(h->pad_a);
+    if (h->pad_b) (void)hipFree(h->pad_b);
+    h->cart = nullptr;
+    h->ep = nullptr;
+    h->pad_s = h->pad_a = h->pad_b = nullptr;
+}
+
+bool aligned4(const void* ptr) { return ((uintptr_t)ptr & 3u) == 0u; }
+
+unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
+
+// Largest padding count of the register-resident (one thread per env) kernel.
+constexpr uint32_t kMaxRegisterWords = 16u;
+
+template <bool REC, bool STATS>
+hipError_t launch_cart(const StepArgs& a, hipStream_t s)
+{
+    const dim3 grid(grid_for(a.n)), block(kBlock);
+    if (a.D == 0u) hipLaunchKernelGGL((k_cartpole_fused<0, REC, STATS>), grid, block, 0, s, a);
+    else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
+    else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+void rlsim_cfg_default(rlsim_cfg* c)
+{
+    if (!c) return;
+    c->gravity = 9.8f;
+    c->masscart = 1.0f;
+    c->masspole = 0.1f;
+    c->half_length = 0.5f;
+    c->force_mag = 10.0f;
+    c->tau = 0.02f;
+    c->x_threshold = 2.4f;
+    c->theta_threshold_rad = (float)(12.0 * 2.0 * 3.14159265358979323846 / 360.0);
+    c->max_episode_steps = 500u;
+    c->reset_low = -0.05f;
+    c->reset_high = 0.05f;
+    c->pad_a_low = 0.9f;
+    c->pad_a_high = 0.99f;
+    c->pad_b_low = -1.0f;
+    c->pad_b_high = 1.0f;
+    c->flags = 0u;
+    c->stream = nullptr;
+}
+
+int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rlsim_t** out)
+{
+    if (!out) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: out is NULL");
+    *out = nullptr;
+    if (n_envs == 0u || n_envs > (1u << 30)) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: n_envs must be in [1, 2^30]");
+    if (state_words < 4u) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: state_words must be >= 4");
+    rlsim_cfg c;
+    if (cfg) c = *cfg;
+    else rlsim_cfg_default(&c);
+    if (const char* why = check_cfg(c)) return fail(nullptr, RLSIM_EINVAL, std::string("rlsim_create: ") + why);
+    const uint32_t D = state_words - 4u;
+    if (D > kMaxRegisterWords)
+        return fail(nullptr, RLSIM_EUNSUPPORTED, "rlsim_create: more than 16 padding words not built yet");
+
+    rlsim* h = new (std::nothrow) rlsim();
+    if (!h) return fail(nullptr, RLSIM_ENOMEM, "rlsim_create: host allocation failed");
+    h->n = n_envs;
+    h->D = D;
+    h->cfg = c;
+    h->stream = (hipStream_t)c.stream;
+    hipError_t e = hipGetDevice(&h->device);
+    if (e != hipSuccess) {
+        int rc = hip_fail(nullptr, e, "rlsim_create: hipGetDevice");
+        delete h;
+        return rc;
+    }
+    const size_t n = n_envs;
+    e = hipMalloc(&h->cart, 4 * n * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&h->ep, n * sizeof(uint32_t));
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_s, (size_t)D * n * sizeof(float));
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_a, (size_t)D * n * sizeof(float));
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_b, (size_t)D * n * sizeof(float));
+    if (e != hipSuccess) {
+        int rc = (e == hipErrorOutOfMemory) ? fail(nullptr, RLSIM_ENOMEM, "rlsim_create: device allocation failed")
+                                            : hip_fail(nullptr, e, "rlsim_create: hipMalloc");
+        (void)hipGetLastError();
+        free_state(h);
+        delete h;
+        return rc;
+    }
+    *out = h;
+    return RLSIM_OK;
+}
+
+int rlsim_reset(rlsim_t* h, uint64_t seed)
+{
+    if (!h) return fail(nullptr, RLSIM_EINVAL, "rlsim_reset: handle is NULL");
+    DeviceGuard g(h->device);
+    if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_reset: cannot select the handle's device");
+    h->dp = make_dev_params(h->cfg, seed);
+    hipLaunchKernelGGL(k_reset_cart, dim3(grid_for(h->n)), dim3(kBlock), 0, h->stream, h->dp, h->n, h->cart, h->ep);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(h, e, "rlsim_reset: launch");
+    if (h->D) {
+        volatile float a_w = h->cfg.pad_a_high - h->cfg.pad_a_low;
+        volatile float b_w = h->cfg.pad_b_high - h->cfg.pad_b_low;
+        const size_t pairs = (size_t)h->n * h->D;
+        const unsigned blocks = (unsigned)std::min<size_t>((pairs + kBlock - 1) / kBlock, 65536);
+        hipLaunchKernelGGL(k_reset_pad, dim3(blocks), dim3(kBlock), 0, h->stream, h->dp, h->n, h->D, (size_t)h->n,
+                           (size_t)1, h->cfg.pad_a_low, (float)a_w, h->cfg.pad_b_low, (float)b_w, h->pad_s,
+                           h->pad_a, h->pad_b);
+        e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(h, e, "rlsim_reset: launch");
+    }
+    h->t = 0;
+    h->has_reset = true;
+    h->err.clear();
+    return RLSIM_OK;
+}
+
+int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const rlsim_traj* traj)
+{
+    if (!h) return fail(nullptr, RLSIM_EINVAL, "rlsim_step_fused: handle is NULL");
+    if (!h->has_reset) return fail(h, RLSIM_ESTATE, "rlsim_step_fused: called before rlsim_reset");
+    if (K == 0u) return fail(h, RLSIM_EINVAL, "rlsim_step_fused: K must be >= 1");
+    if (h->t + (uint64_t)K > 0xFFFFFFFFull) return fail(h, RLSIM_EINVAL, "rlsim_step_fused: global step would pass 2^32 - 1");
+    rlsim_traj tr{};
+    if (traj) tr = *traj;
+    const int n_set = (tr.obs != nullptr) + (tr.action != nullptr) + (tr.reward != nullptr) + (tr.done != nullptr);
+    if (n_set != 0 && n_set != 4)
+        return fail(h, RLSIM_EINVAL, "rlsim_step_fused: obs, action, reward and done must be all set or all NULL");
+    if (!aligned4(tr.obs) || !aligned4(tr.reward) || !aligned4(tr.block_stats) || !aligned4(tr.policy_p0))
+        return fail(h, RLSIM_EINVAL, "rlsim_step_fused: f32/u32 pointers must be 4-byte aligned");
+    if (tr.policy_p0 && !policy) return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy_p0 needs a policy");
+    if (policy) return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: policy kernels not built yet");
+
+    DeviceGuard g(h->device);
+    if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_step_fused: cannot select the handle's device");
+    StepArgs a{};
+    a.p = h->dp;
+    a.n = h->n;
+    a.D = h->D;
+    a.t0 = (uint32_t)h->t;
+    a.K = K;
+    a.cart = h->cart;
+    a.ep = h->ep;
+    a.pad_s = h->pad_s;
+    a.pad_a = h->pad_a;
+    a.pad_b = h->pad_b;
+    a.obs = tr.obs;
+    a.action = tr.action;
+    a.reward = tr.reward;
+    a.done = tr.done;
+    a.stats = tr.block_stats;
+    const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
+    hipError_t e;
+    if (rec && stats) e = launch_cart<true, true>(a, h->stream);
+    else if (rec) e = launch_cart<true, false>(a, h->stream);
+    else if (stats) e = launch_cart<false, true>(a, h->stream);
+    else e = launch_cart<false, false>(a, h->stream);
+    if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");
+    h->t += K;
+    return RLSIM_OK;
+}
+
+int rlsim_get_state(rlsim_t* h, float* host_state, uint32_t* host_ep, uint64_t* t_out)
+{
+    if (!h) return fail(nullptr, RLSIM_EINVAL, "rlsim_get_state: handle is NULL");
+    if (!h->has_reset) return fail(h, RLSIM_ESTATE, "rlsim_get_state: called before rlsim_reset");
+    DeviceGuard g(h->device);
+    if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_get_state: cannot select the handle's device");
+    const size_t n = h->n;
+    hipError_t e = hipSuccess;
+    if (host_state) {
+        e = hipMemcpyAsync(host_state, h->cart, 4 * n * sizeof(float), hipMemcpyDeviceToHost, h->stream);
+        if (e == hipSuccess && h->D)
+            e = hipMemcpyAsync(host_state + 4 * n, h->pad_s, (size_t)h->D * n * sizeof(float), hipMemcpyDeviceToHost,
+                               h->stream);
+    }
+    if (e == hipSuccess && host_ep) e = hipMemcpyAsync(host_ep, h->ep, n * sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e != hipSuccess) return hip_fail(h, e, "rlsim_get_state");
+    if (t_out) *t_out = h->t;
+    return RLSIM_OK;
+}
+
+int rlsim_set_state(rlsim_t* h, const float* host_state, const uint32_t* host_ep, uint64_t t)
+{
+    if (!h) return fail(nullptr, RLSIM_EINVAL, "rlsim_set_state: handle is NULL");
+    if (!h->has_reset) return fail(h, RLSIM_ESTATE, "rlsim_set_state: called before rlsim_reset");
+    if (t > 0xFFFFFFFFull) return fail(h, RLSIM_EINVAL, "rlsim_set_state: t must be <= 2^32 - 1");
+    DeviceGuard g(h->device);
+    if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_set_state: cannot select the handle's device");
+    const size_t n = h->n;
+    hipError_t e = hipSuccess;
+    if (host_state) {
+        e = hipMemcpyAsync(h->cart, host_state, 4 * n * sizeof(float), hipMemcpyHostToDevice, h->stream);
+        if (e == hipSuccess && h->D)
+            e = hipMemcpyAsync(h->pad_s, host_state + 4 * n, (size_t)h->D * n * sizeof(float), hipMemcpyHostToDevice,
+                               h->stream);
+    }
+    if (e == hipSuccess && host_ep) e = hipMemcpyAsync(h->ep, host_ep, n * sizeof(uint32_t), hipMemcpyHostToDevice, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e != hipSuccess) return hip_fail(h, e, "rlsim_set_state");
+    h->t = t;
+    return RLSIM_OK;
+}
+
+int rlsim_destroy(rlsim_t* h)
+{
+    if (!h) return RLSIM_OK;
+    int rc = RLSIM_OK;
+    {
+        DeviceGuard g(h->device);
+        hipError_t e = hipStreamSynchronize(h->stream);
+        if (e != hipSuccess) rc = RLSIM_EDEVICE;
+        free_state(h);
+    }
+    delete h;
+    return rc;
+}
+
+const char* rlsim_last_error(const rlsim_t* h)
+{
+    return h ? h->err.c_str() : g_create_err.c_str();
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+"""Shared helpers of the GPU tests: run the HIP library and the CPU oracle on the
+same seeded workload and return host arrays."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+import workloads
+
+
+def oracle_run(n, T, K_schedule, D=0, seed=0, env0=0, cfg=None, policy=None):
+    """Oracle trajectory for envs env0..env0+n-1 over T steps, split into calls
+    of the given sizes (stats kept per call)."""
+    params = oracle.make_params(**(cfg or workloads.CARTPOLE))
+    sim = oracle.Sim(n, D, params, env0=env0)
+    sim.reset(seed)
+    parts = [sim.step(k, policy=policy) for k in K_schedule]
+    assert sum(K_schedule) == T
+    out = {key: np.concatenate([p[key] for p in parts]) for key in ("obs", "action", "reward", "done")}
+    if policy is not None:
+        out["p0"] = np.concatenate([p["p0"] for p in parts])
+    out["stats"] = [p["stats"] for p in parts]
+    out["state"], out["ep"], out["t"] = sim.get_state()
+    return out
+
+
+def gpu_run(n, T, K_schedule, D=0, seed=0, cfg=None, stats=True, stream=None, policy=None, p0=False,
+            slices=None):
+    """GPU trajectory over T steps with the given K schedule.  Returns host
+    arrays; if ``slices`` (list of (start, stop) env ranges) is given, only
+    those columns are copied back (for full-size runs)."""
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+
+    sim = Simulator(n, D, cfg or workloads.CARTPOLE, stream=stream)
+    try:
+        sim.reset(seed)
+        traj = Trajectory(T, n, stats=stats, p0=p0)
+        stats_list = []
+        k0 = 0
+        for k in K_schedule:
+            sim.step(k, traj.rows(k0, k), policy=policy)
+            if stats:
+                stats_list.append(traj.block_stats.clone())
+            k0 += k
+        assert k0 == T
+        torch.cuda.synchronize()
+        state, ep, t = sim.get_state()
+
+        def cols(x):
+            if slices is None:
+                return x.cpu().numpy()
+            return np.concatenate([x[..., a:b].cpu().numpy() for a, b in slices], axis=-1)
+
+        out = dict(obs=cols(traj.obs), action=cols(traj.action), reward=cols(traj.reward), done=cols(traj.done))
+        if p0:
+            out["p0"] = cols(traj.policy_p0)
+        out["stats"] = [s.cpu().numpy().view(np.uint32) for s in stats_list]
+        if slices is None:
+            out["state"], out["ep"] = state, ep
+        else:
+            out["state"] = np.concatenate([state[:, a:b] for a, b in slices], axis=1)
+            out["ep"] = np.concatenate([ep[a:b] for a, b in slices])
+        out["t"] = t
+        del traj
+        return out
+    finally:
+        sim.close()
+
+
+def assert_bit_equal(gpu, ref, keys=("obs", "action", "reward", "done", "state", "ep")):
+    for key in keys:
+        g, r = np.asarray(gpu[key]), np.asarray(ref[key])
+        assert g.shape == r.shape, (key, g.shape, r.shape)
+        if g.dtype.kind == "f":
+            same = (g.view(np.uint32) == r.view(np.uint32)) | (np.isnan(g) & np.isnan(r))
+        else:
+            same = g == r
+        if not np.all(same):
+            idx = np.argwhere(~same)[0]
+            raise AssertionError(f"{key} differs first at {tuple(idx)}: gpu {g[tuple(idx)]!r} oracle {r[tuple(idx)]!r} "
+                                 f"({int((~same).sum())} of {same.size} differ)")
+    assert gpu["t"] == ref["t"]

@@ -1,0 +1,152 @@
+"""The C ABI: symbols, defaults and argument checks.
+
+CPU tests load librlsim.so and check that it exports every function
+include/rlsim.h declares and rejects bad arguments that need no device.  GPU
+tests cover the error paths that need a live handle.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rlsim.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rlsim_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2207_07736_amd as p
+    names = _declared()
+    assert set(names) == set(p.EXPORTS), names
+    lib = ctypes.CDLL(p.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+    nm = subprocess.run(["nm", "-D", "--defined-only", p.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (rlsim_\w+)", nm))
+    assert exported == set(names)
+    assert "orc_" not in nm                      # the oracle is never linked in
+
+
+def test_product_does_not_reach_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2207_07736_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text and "orc_" not in text, f
+
+
+def test_cfg_default_matches_workload_constants():
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    for k, v in workloads.CARTPOLE.items():
+        if k == "no_termination":
+            assert c.flags == 0
+            continue
+        got = getattr(c, k)
+        want = np.float32(v) if isinstance(v, float) else v
+        assert np.float32(got) == want if isinstance(v, float) else got == want, k
+    assert np.float32(c.theta_threshold_rad).view(np.uint32) == 0x3E567750
+    assert c.stream is None
+
+
+@pytest.mark.parametrize("n,words", [(0, 4), (1 << 30 | 1, 4), (16, 3), (16, 0)])
+def test_create_rejects_bad_sizes(n, words):
+    import paper_2207_07736_amd as p
+    with pytest.raises(p.RlsimError) as e:
+        p.rlsim_create(n, words)
+    assert e.value.code == p.RLSIM_EINVAL
+    assert p.rlsim_last_error(None)
+
+
+@pytest.mark.parametrize("field,value", [("masscart", 0.0), ("half_length", -1.0), ("tau", float("nan")),
+                                         ("reset_low", 1.0), ("gravity", float("inf"))])
+def test_create_rejects_bad_cfg(field, value):
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    setattr(c, field, value)
+    with pytest.raises(p.RlsimError) as e:
+        p.rlsim_create(8, 4, c)
+    assert e.value.code == p.RLSIM_EINVAL
+
+
+def test_create_rejects_unknown_flags_and_null_out():
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    c.flags = 0x10
+    with pytest.raises(p.RlsimError):
+        p.rlsim_create(8, 4, c)
+    assert p.lib.rlsim_create(8, 4, None, None) == p.RLSIM_EINVAL
+
+
+def test_null_handle_calls():
+    import paper_2207_07736_amd as p
+    L = p.lib
+    assert L.rlsim_destroy(None) == p.RLSIM_OK
+    assert L.rlsim_reset(None, 0) == p.RLSIM_EINVAL
+    assert L.rlsim_step_fused(None, 1, None, None) == p.RLSIM_EINVAL
+    assert L.rlsim_get_state(None, None, None, None) == p.RLSIM_EINVAL
+    assert L.rlsim_set_state(None, None, None, 0) == p.RLSIM_EINVAL
+    L.rlsim_cfg_default(None)
+
+
+# ---------------------------------------------------------------- GPU error paths
+@pytest.mark.gpu
+def test_state_and_argument_errors_with_handle():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2207_07736_amd as p
+    sim = p.Simulator(300, 0, workloads.CARTPOLE)
+    try:
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(1)
+        assert e.value.code == p.RLSIM_ESTATE
+        with pytest.raises(p.RlsimError) as e:
+            sim.get_state()
+        assert e.value.code == p.RLSIM_ESTATE
+        sim.reset(0)
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(0)
+        assert e.value.code == p.RLSIM_EINVAL
+        tr = p.Trajectory(4, 300)
+        bad = p.traj_struct(obs=tr.obs, action=tr.action)          # mixed NULLs
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(4, bad)
+        assert e.value.code == p.RLSIM_EINVAL
+        mis = p.rlsim_traj(tr.obs.data_ptr() + 2, tr.action.data_ptr(), tr.reward.data_ptr(), tr.done.data_ptr(),
+                           None, None)
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(4, mis)
+        assert e.value.code == p.RLSIM_EINVAL
+        p0only = p.traj_struct(policy_p0=tr.obs)
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(4, p0only)
+        assert e.value.code == p.RLSIM_EINVAL
+        st, ep, t = sim.get_state()
+        sim.set_state(st, ep, 2**32 - 5)
+        sim.step(4)
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(1)
+        assert e.value.code == p.RLSIM_EINVAL
+        with pytest.raises(p.RlsimError) as e:
+            sim.set_state(None, None, 2**32)
+        assert e.value.code == p.RLSIM_EINVAL
+        # a failed call leaves the handle usable
+        sim.set_state(None, None, 0)
+        sim.step(4, tr.rows(0, 4))
+        torch.cuda.synchronize()
+        assert int(tr.action.max()) <= 1
+        del tr
+    finally:
+        sim.close()

@@ -1,0 +1,241 @@
+"""GPU parity: the HIP library against the CPU oracle, through the C ABI.
+
+Random-action runs are compared bit for bit: observations, actions, rewards,
+done bytes, block statistics, the final state (cart-pole and padding words),
+the episode counters and the global step.  Sizes span several 256-env tiles
+and ragged tails; the full-size workloads are compared on sampled env slices
+(oracle on the same global env ids) plus properties that hold at any size.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_helpers import assert_bit_equal, gpu_run, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2207_07736_amd  # noqa: F401  (fails loudly if the library is missing)
+
+
+def _stats_equal(g, r):
+    assert len(g) == len(r)
+    for a, b in zip(g, r):
+        assert np.array_equal(a, b)
+
+
+def test_c1_full_bit_exact():
+    """1,024 envs, 100 steps, one launch per step (the unfused form), seed 0."""
+    w = workloads.WORKLOADS["C1"]
+    sched = [1] * w["T"]
+    g = gpu_run(w["n"], w["T"], sched, seed=w["seed"])
+    r = oracle_run(w["n"], w["T"], sched, seed=w["seed"])
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+    assert r["done"].any()          # episodes do end within the run
+
+
+@pytest.mark.parametrize("seed", workloads.PARITY_SEEDS)
+@pytest.mark.parametrize("n", [1, 257, 1000])
+def test_ragged_sizes_and_seeds(n, seed):
+    T = 150
+    sched = [1, 6, 57, 86]                       # unaligned call boundaries
+    g = gpu_run(n, T, sched, seed=seed)
+    r = oracle_run(n, T, sched, seed=seed)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
+@pytest.mark.parametrize("sched", [[300], [1] * 300, [7] * 42 + [6], [128, 129, 43]])
+def test_k_partitions_match_oracle(sched):
+    n, T = 700, 300
+    g = gpu_run(n, T, sched, seed=1)
+    r = oracle_run(n, T, [T], seed=1)
+    assert_bit_equal(g, r)
+
+
+@pytest.mark.parametrize("D", [1, 4, 5, 16])
+def test_padding_words_bit_exact(D):
+    n, T = 513, 260
+    sched = [100, 160]
+    g = gpu_run(n, T, sched, D=D, seed=2)
+    r = oracle_run(n, T, sched, D=D, seed=2)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
+@pytest.mark.parametrize("overrides", [
+    dict(max_episode_steps=5),
+    dict(max_episode_steps=0, no_termination=1),
+    dict(max_episode_steps=3, x_threshold=0.01),        # terminated and truncated together
+    dict(max_episode_steps=1),
+    dict(force_mag=0.0, gravity=0.0),
+])
+def test_edge_configs(overrides):
+    cfg = workloads.cartpole(**overrides)
+    n, T = 300, 120
+    g = gpu_run(n, T, [50, 70], D=2, seed=3, cfg=cfg)
+    r = oracle_run(n, T, [50, 70], D=2, seed=3, cfg=cfg)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
+def test_c2_k_sweep_full_size():
+    """65,536 envs x 1,000 steps: K = 1, 10, 100 and 1,000 give the identical
+    trajectory; sampled slices equal the oracle."""
+    w = workloads.WORKLOADS["C2"]
+    n, T = w["n"], w["T"]
+    slices = [(0, 256), (30000, 30100), (n - 256, n)]
+    outs = {K: gpu_run(n, T, [K] * (T // K), seed=w["seed"], slices=slices) for K in w["K"]}
+    base = outs[1000]
+    for K, o in outs.items():
+        assert_bit_equal(o, base)
+    ref = [oracle_run(b - a, T, [T], seed=w["seed"], env0=a) for a, b in slices]
+    merged = {key: np.concatenate([x[key] for x in ref], axis=-1) for key in ("obs", "action", "reward", "done", "state")}
+    merged["ep"] = np.concatenate([x["ep"] for x in ref])
+    merged["t"] = T
+    assert_bit_equal(base, merged)
+
+
+def test_c3_headline_sampled_and_properties():
+    """4,194,304 envs x 200 steps in one launch (K = 200), as the bench times it."""
+    w = workloads.WORKLOADS["C3"]
+    n, T = w["n"], w["T"]
+    slices = [(0, 256), (2097152, 2097152 + 256), (n - 512, n)]
+    g = gpu_run(n, T, [T], seed=w["seed"], slices=slices)
+    ref = [oracle_run(b - a, T, [T], seed=w["seed"], env0=a) for a, b in slices]
+    merged = {key: np.concatenate([x[key] for x in ref], axis=-1) for key in ("obs", "action", "reward", "done", "state")}
+    merged["ep"] = np.concatenate([x["ep"] for x in ref])
+    merged["t"] = T
+    assert_bit_equal(g, merged)
+    # block statistics of the sampled blocks
+    blocks = [0, 2097152 // 256, n // 256 - 2, n // 256 - 1]
+    want = np.concatenate([ref[0]["stats"][0], ref[1]["stats"][0], ref[2]["stats"][0]])
+    assert np.array_equal(g["stats"][0][blocks], want)
+
+
+def test_c3_whole_batch_properties():
+    """Properties of the full headline trajectory that hold at any size: every
+    reward is 1, actions are bits, done bytes are in {0..3}, the block statistics
+    count exactly the done bytes, and stored episode counters stay below 500."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C3"]
+    n, T = w["n"], w["T"]
+    sim = Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(w["seed"])
+        traj = Trajectory(T, n)
+        sim.step(T, traj.rows(0, T))
+        torch.cuda.synchronize()
+        assert bool((traj.reward == 1.0).all())
+        assert int(traj.action.max()) <= 1
+        assert int(traj.done.max()) <= 3
+        dn = traj.done.to(torch.int64)
+        per_env = (dn != 0).sum(dim=0)
+        per_block = per_env.view(-1, 256).sum(dim=1)
+        stats = traj.block_stats.to(torch.int64)
+        assert torch.equal(stats[:, 0], per_block)
+        assert torch.equal(stats[:, 2], (dn & 1).sum(dim=0).view(-1, 256).sum(dim=1))
+        assert torch.equal(stats[:, 3], (dn >> 1).sum(dim=0).view(-1, 256).sum(dim=1))
+        _, ep, t = sim.get_state()
+        assert t == T and int(ep.max()) < 500
+        # fraction of env-steps that end an episode: ~1/22 for random pushes
+        frac = float(per_env.sum()) / (n * T)
+        assert 0.035 < frac < 0.055
+        del traj
+    finally:
+        sim.close()
+
+
+def test_rerun_deterministic_and_stream():
+    n, T = 4096, 64
+    s = torch.cuda.Stream()
+    a = gpu_run(n, T, [T], seed=5, stream=s)
+    b = gpu_run(n, T, [32, 32], seed=5)
+    assert_bit_equal(a, b)
+
+
+def test_no_trajectory_and_stats_only():
+    from paper_2207_07736_amd import Simulator, traj_struct
+    n, T = 1000, 90
+    r = oracle_run(n, T, [T], seed=4)
+    sim = Simulator(n, 3, workloads.CARTPOLE)
+    try:
+        sim.reset(4)
+        sim.step(T, None)                       # traj NULL: pure simulation
+        st_a, ep_a, t_a = sim.get_state()
+        sim.reset(4)
+        stats = torch.zeros(((n + 255) // 256, 4), dtype=torch.int32, device="cuda")
+        sim.step(T, traj_struct(block_stats=stats))
+        st_b, ep_b, _ = sim.get_state()
+    finally:
+        sim.close()
+    r3 = oracle_run(n, T, [T], D=3, seed=4)
+    assert np.array_equal(st_a.view(np.uint32), r3["state"].view(np.uint32)) and np.array_equal(ep_a, r3["ep"])
+    assert np.array_equal(st_b.view(np.uint32), r3["state"].view(np.uint32)) and t_a == T
+    assert np.array_equal(stats.cpu().numpy().view(np.uint32), r3["stats"][0])
+    assert r["done"].any()
+
+
+def test_get_set_state_resume():
+    from paper_2207_07736_amd import Simulator, Trajectory
+    n, T, D = 777, 140, 4
+    whole = gpu_run(n, T, [T], D=D, seed=8)
+    sim = Simulator(n, D, workloads.CARTPOLE)
+    sim2 = Simulator(n, D, workloads.CARTPOLE)
+    try:
+        sim.reset(8)
+        tr1 = Trajectory(T // 2, n)
+        sim.step(T // 2, tr1.rows(0, T // 2))
+        st, ep, t = sim.get_state()
+        sim2.reset(8)                              # same padding parameters
+        sim2.set_state(st, ep, t)
+        tr2 = Trajectory(T - T // 2, n)
+        sim2.step(T - T // 2, tr2.rows(0, T - T // 2))
+        torch.cuda.synchronize()
+        obs = np.concatenate([tr1.obs.cpu().numpy(), tr2.obs.cpu().numpy()])
+        done = np.concatenate([tr1.done.cpu().numpy(), tr2.done.cpu().numpy()])
+        assert np.array_equal(obs.view(np.uint32), whole["obs"].view(np.uint32))
+        assert np.array_equal(done, whole["done"])
+        st2, ep2, t2 = sim2.get_state()
+        assert np.array_equal(st2.view(np.uint32), whole["state"].view(np.uint32)) and t2 == T
+    finally:
+        sim.close()
+        sim2.close()
+
+
+def test_nan_state_propagates_like_oracle():
+    """A NaN injected through set_state never crosses a threshold (NaN compares
+    false), so the env runs to the time limit; both sides agree on NaN-ness."""
+    import oracle
+    from paper_2207_07736_amd import Simulator, Trajectory
+    n, T = 300, 40
+    cfg = workloads.cartpole(max_episode_steps=30)
+    sim = Simulator(n, 0, cfg)
+    osim = oracle.Sim(n, 0, oracle.make_params(**cfg))
+    try:
+        sim.reset(1)
+        osim.reset(1)
+        st, ep, t = sim.get_state()
+        st[2, 5] = np.nan
+        st[0, 100] = np.inf
+        sim.set_state(st, ep, t)
+        osim.set_state(st, ep, t)
+        tr = Trajectory(T, n)
+        sim.step(T, tr.rows(0, T))
+        torch.cuda.synchronize()
+        ref = osim.step(T)
+        g_done = tr.done.cpu().numpy()
+        assert np.array_equal(g_done, ref["done"])
+        g_obs = tr.obs.cpu().numpy()
+        assert np.array_equal(np.isnan(g_obs), np.isnan(ref["obs"]))
+        fin = ~np.isnan(g_obs)
+        assert np.array_equal(g_obs[fin].view(np.uint32), ref["obs"][fin].view(np.uint32))
+    finally:
+        sim.close()
