@@ -74,6 +74,74 @@ def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
                       f"(seed {seed}, trajectory recorded), {elapsed:.1f} s"}
 
 
+def _time_schedule(sim, traj, sched, stream, reps):
+    """Median wall time (ms, HIP events) of running the K schedule `sched`
+    (one launch per entry, trajectory rows advanced) over `reps` repetitions."""
+    import torch
+    structs, k0 = [], 0
+    for k in sched:
+        structs.append((k, traj.rows(k0, k) if traj is not None else None))
+        k0 += k
+    times = []
+    for r in range(reps + 1):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for k, st in structs:
+            sim.step(k, st)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        if r:                       # the first repetition is a warm-up
+            times.append(start.elapsed_time(stop))
+    times.sort()
+    return times[len(times) // 2]
+
+
+def fusion_sweeps(stream) -> dict:
+    """Fused versus unfused on the K sweep (65,536 envs x 1,000 steps) and the
+    state-size sweep (262,144 envs x 500 steps, D padding words per env)."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    out = {}
+    w = workloads.WORKLOADS["C2"]
+    n, T = w["n"], w["T"]
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    rows = {}
+    for K in w["K"]:
+        ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=3)
+        rows[str(K)] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3)}
+    base = rows["1"]["ms"]
+    for r in rows.values():
+        r["speedup_vs_K1"] = base / r["ms"]
+    out[w["name"]] = rows
+    del traj
+    sim.close()
+
+    w = workloads.WORKLOADS["C4"]
+    n, T = w["n"], w["T"]
+    d_rows = {}
+    for D in w["D"]:
+        sim = Simulator(n, D, workloads.CARTPOLE, stream=stream)
+        sim.reset(w["seed"])
+        traj = Trajectory(T, n)
+        entry = {}
+        for K in w["K"]:
+            ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=2)
+            state_bytes = (40 + 16 * D) * n * (T // K)
+            entry[f"K{K}"] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3),
+                              "algorithmic_GBs": (n * T * workloads.TRAJ_BYTES_PER_ENV_STEP + state_bytes) / (ms * 1e-3) / 1e9}
+        ms_nt = _time_schedule(sim, None, [T], stream, reps=2)
+        entry["K500_no_trajectory"] = {"ms": ms_nt, "env_steps_per_s": n * T / (ms_nt * 1e-3)}
+        entry["fusion_speedup"] = entry["K1"]["ms"] / entry["K500"]["ms"]
+        d_rows[f"D{D}"] = entry
+        del traj
+        sim.close()
+        print(f"[bench] sweep D={D}: K1 {entry['K1']['ms']:.2f} ms, K500 {entry['K500']['ms']:.2f} ms", file=sys.stderr,
+              flush=True)
+    out[w["name"]] = d_rows
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,6 +149,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-unfused", action="store_true", help="skip the K=1 contrast")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the K and state-size sweeps")
     ap.add_argument("--cpu-slice-envs", type=int, default=65536)
     ap.add_argument("--cpu-slices", type=int, default=8)
     args = ap.parse_args()
@@ -175,6 +244,9 @@ def main() -> int:
 
     del traj
     sim.close()
+
+    if not args.no_sweep:
+        result["sweeps"] = fusion_sweeps(stream)
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(args.cpu_slice_envs, args.cpu_slices, T, seed)

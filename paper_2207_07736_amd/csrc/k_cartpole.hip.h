@@ -1,5 +1,13 @@
-// k_cartpole.hip.h -- the fused K-step simulator kernel, one thread per
-// environment, random actions, up to W padding words held in registers.
+// k_cartpole.hip.h -- fused K-step simulator kernels with random actions.
+//
+//  k_cartpole_fused<W>: one thread per environment; the cart-pole state and up
+//      to W padding words stay in registers for all K steps.
+//  k_cartpole_wide<G,W>: wide padding (the paper's state-size factor): phase 1
+//      runs the cart-pole steps one thread per environment and leaves each
+//      step's (action, done) bits in LDS; phase 2 gives every environment G
+//      lanes holding W padding words each in registers and replays the steps
+//      from those bits.  The padding words only feed on (action, done), so the
+//      split is exact, and each word is still read and written once per launch.
 #pragma once
 
 #include "device_common.hip.h"
@@ -11,14 +19,15 @@ constexpr int kBlock = 256;          // threads per workgroup = envs per stats b
 struct StepArgs {
     DevParams p;
     uint32_t n;          // environments
-    uint32_t D;          // padding words (<= W of the instantiation)
+    uint32_t D;          // padding words
+    uint32_t Dp;         // padded row length of the wide layout (multiple of 4)
     uint32_t t0;         // global step of row 0
     uint32_t K;          // steps in this launch
     float* cart;         // [4][n]   x, x_dot, theta, theta_dot
     uint32_t* ep;        // [n]      steps taken in the current episode
-    float* pad_s;        // [D][n]   padding words
-    const float* pad_a;  // [D][n]
-    const float* pad_b;  // [D][n]
+    float* pad_s;        // narrow: [D][n]; wide: [n][Dp]
+    const float* pad_a;
+    const float* pad_b;
     float* obs;          // [K][4][n]
     uint8_t* action;     // [K][n]
     float* reward;       // [K][n]
@@ -26,148 +35,371 @@ struct StepArgs {
     uint32_t* stats;     // [ceil(n/256)][4]
 };
 
-// Words of the action block that holds step t: the 32 action bits of steps
-// t & ~31 .. (t & ~31) + 31, least significant first.
+// The word of an action block that holds the 32 action bits of steps
+// 32q .. 32q+31 (least significant bit first).
 __device__ __forceinline__ uint32_t pick_word(const uint4& w, uint32_t q)
 {
     return q == 0u ? w.x : q == 1u ? w.y : q == 2u ? w.z : w.w;
 }
 
-// Fused K-step loop.  The state of one environment lives in registers for all
-// K steps; per step the only device-memory traffic is the trajectory row
-// (22 bytes).  RNG words are drawn once per block of steps: one Philox call per
-// 128 steps for the actions, one per 4 steps for the reset draw that an episode
-// ending in that block would start from.
+// Hides a per-lane 32-bit offset from loop strength reduction, so that a store
+// is addressed as (scalar 64-bit row base) + (per-lane 32-bit offset) rather
+// than through a per-lane 64-bit pointer advanced every step.
+__device__ __forceinline__ uint32_t opaque(uint32_t v)
+{
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// One environment's cart-pole state and RNG words, advanced step by step.
+template <bool REC, bool STATS>
+struct CartCore {
+    const DevParams& p;
+    uint32_t env;
+    CartState s;
+    uint32_t ep;
+    uint4 aw;            // action words of the current 128-step block
+    uint32_t abits;      // remaining action bits of the current 32-step word
+    CartState rs;        // reset draw for an episode beginning in the current 4-step block
+    float* obs;          // trajectory row pointers (wave-uniform)
+    uint8_t* act_row;
+    float* rew_row;
+    uint8_t* done_row;
+    size_t plane;
+    uint32_t n_eps = 0u, n_len = 0u, n_term = 0u, n_trunc = 0u;
+
+    __device__ __forceinline__ CartCore(const DevParams& p_, uint32_t env_) : p(p_), env(env_) {}
+
+    __device__ __forceinline__ void draw_reset(uint32_t block)
+    {
+        const uint4 w = philox(env, block, STREAM_RESET, p.key0, p.key1);
+        rs.x = uniform01_to(w.x, p.reset_lo, p.reset_width);
+        rs.xd = uniform01_to(w.y, p.reset_lo, p.reset_width);
+        rs.th = uniform01_to(w.z, p.reset_lo, p.reset_width);
+        rs.thd = uniform01_to(w.w, p.reset_lo, p.reset_width);
+    }
+
+    // Called before the step at t when t is a multiple of 32.
+    __device__ __forceinline__ void refresh_actions(uint32_t t)
+    {
+        if ((t & 127u) == 0u) aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
+        abits = pick_word(aw, (t >> 5) & 3u);
+    }
+
+    // Step t.  hook(act, reset) sees the action and whether the episode ended.
+    template <class Hook>
+    __device__ __forceinline__ void step(Hook& hook)
+    {
+        const uint32_t act = abits & 1u;
+        abits >>= 1;
+        const CartState nx = cartpole_step(p, s, act);
+        const uint32_t len = ep + 1u;
+        const uint32_t term = crossed(p, nx);
+        const uint32_t trunc = (uint32_t)((p.max_steps != 0u) & (len >= p.max_steps));
+        const uint32_t d = term | (trunc << 1);
+        if (REC) {
+            const uint32_t o4 = opaque(env * 4u), o1 = opaque(env);
+            *at(obs, o4) = s.x;
+            *at(obs + plane, o4) = s.xd;
+            *at(obs + 2 * plane, o4) = s.th;
+            *at(obs + 3 * plane, o4) = s.thd;
+            *at(act_row, o1) = (uint8_t)act;
+            *at(rew_row, o4) = 1.0f;
+            *at(done_row, o1) = (uint8_t)d;
+            obs += 4 * plane;
+            act_row += plane;
+            rew_row += plane;
+            done_row += plane;
+        }
+        const bool reset = d != 0u;
+        s.x = reset ? rs.x : nx.x;
+        s.xd = reset ? rs.xd : nx.xd;
+        s.th = reset ? rs.th : nx.th;
+        s.thd = reset ? rs.thd : nx.thd;
+        ep = reset ? 0u : len;
+        hook(act, reset);
+        if (STATS) {
+            n_eps += reset ? 1u : 0u;
+            n_len += reset ? len : 0u;
+            n_term += term;
+            n_trunc += trunc;
+        }
+    }
+
+    // Steps t0 .. t0+K-1.  The loop body covers the four steps that share one
+    // reset block ((t+1)/4 constant), so each reset draw is computed once, at a
+    // fixed place, and the body has no data-dependent control flow.
+    template <class Hook>
+    __device__ __forceinline__ void run(uint32_t t0, uint32_t K, Hook& hook)
+    {
+        uint32_t t = t0, k = 0;
+        aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
+        abits = pick_word(aw, (t >> 5) & 3u) >> (t & 31u);
+        if (((t + 1u) & 3u) != 0u) {
+            // up to three steps before the first block boundary; none of them
+            // starts a 32-step action word (they are not multiples of 4)
+            draw_reset((t + 1u) >> 2);
+            while (k < K && ((t + 1u) & 3u) != 0u) {
+                step(hook);
+                ++t;
+                ++k;
+            }
+        }
+        // here t = 4m - 1: steps t .. t+3 draw resets from block m
+        for (; K - k >= 4u; k += 4u, t += 4u) {
+            draw_reset((t + 1u) >> 2);
+            step(hook);
+            if (((t + 1u) & 31u) == 0u) refresh_actions(t + 1u);
+            step(hook);
+            step(hook);
+            step(hook);
+        }
+        if (k < K) {
+            draw_reset((t + 1u) >> 2);
+            step(hook);
+            ++t;
+            ++k;
+            if (k < K) {
+                if ((t & 31u) == 0u) refresh_actions(t);
+                step(hook);
+                ++k;
+                if (k < K) step(hook);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void set_rows(const StepArgs& a, uint32_t k0)
+    {
+        plane = a.n;
+        obs = a.obs + (size_t)k0 * 4 * plane;
+        act_row = a.action + (size_t)k0 * plane;
+        rew_row = a.reward + (size_t)k0 * plane;
+        done_row = a.done + (size_t)k0 * plane;
+    }
+
+    __device__ __forceinline__ void load(const StepArgs& a)
+    {
+        const size_t pl = a.n;
+        s.x = a.cart[env];
+        s.xd = a.cart[pl + env];
+        s.th = a.cart[2 * pl + env];
+        s.thd = a.cart[3 * pl + env];
+        ep = a.ep[env];
+    }
+
+    __device__ __forceinline__ void store(const StepArgs& a)
+    {
+        const size_t pl = a.n;
+        a.cart[env] = s.x;
+        a.cart[pl + env] = s.xd;
+        a.cart[2 * pl + env] = s.th;
+        a.cart[3 * pl + env] = s.thd;
+        a.ep[env] = ep;
+    }
+};
+
+// Sums the four episode counters over the workgroup and writes one row of the
+// block statistics (all threads of the block must call this).
+__device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3)
+{
+    __shared__ uint32_t part[kBlock / 64][4];
+    const uint32_t v0 = wave_sum(c0), v1 = wave_sum(c1), v2 = wave_sum(c2), v3 = wave_sum(c3);
+    const uint32_t wave = threadIdx.x / 64u, lane = threadIdx.x % 64u;
+    if (lane == 0u) {
+        part[wave][0] = v0;
+        part[wave][1] = v1;
+        part[wave][2] = v2;
+        part[wave][3] = v3;
+    }
+    __syncthreads();
+    if (threadIdx.x < 4u) {
+        uint32_t sum = 0u;
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) sum += part[w][threadIdx.x];
+        stats[(size_t)blockIdx.x * 4u + threadIdx.x] = sum;
+    }
+}
+
+// Padding words held by one thread: s <- a s + (act ? b : +0), rounded once;
+// zeroed when the episode ends.
+template <int W>
+struct RegisterPad {
+    float s[W > 0 ? W : 1], a[W > 0 ? W : 1], b[W > 0 ? W : 1];
+    __device__ __forceinline__ void operator()(uint32_t act, bool reset)
+    {
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            const float v = __builtin_fmaf(a[j], s[j], act ? b[j] : 0.0f);
+            s[j] = reset ? 0.0f : v;
+        }
+    }
+};
+
 template <int W, bool REC, bool STATS>
 __global__ __launch_bounds__(kBlock) void k_cartpole_fused(StepArgs a)
 {
     const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
-    const bool live = env < a.n;
-    const DevParams& p = a.p;
-    uint32_t n_eps = 0u, n_len = 0u, n_term = 0u, n_trunc = 0u;
-
-    if (live) {
-        const uint32_t off = env * 4u;              // byte offset of a f32 column (n <= 2^30)
-        const size_t plane = a.n;                   // entries per f32 plane
-        float* const c0 = a.cart;
-        float* const c1 = a.cart + plane;
-        float* const c2 = a.cart + 2 * plane;
-        float* const c3 = a.cart + 3 * plane;
-        CartState s;
-        s.x = *at(c0, off);
-        s.xd = *at(c1, off);
-        s.th = *at(c2, off);
-        s.thd = *at(c3, off);
-        uint32_t ep = a.ep[env];
-
-        float ps[W > 0 ? W : 1], pa[W > 0 ? W : 1], pb[W > 0 ? W : 1];
+    CartCore<REC, STATS> core(a.p, env);
+    if (env < a.n) {
+        core.load(a);
+        if (REC) core.set_rows(a, 0);
+        RegisterPad<W> pad;
 #pragma unroll
         for (int j = 0; j < W; ++j) {
             const bool on = (uint32_t)j < a.D;
             const size_t q = (size_t)j * a.n + env;
-            ps[j] = on ? a.pad_s[q] : 0.0f;
-            pa[j] = on ? a.pad_a[q] : 0.0f;
-            pb[j] = on ? a.pad_b[q] : 0.0f;
+            pad.s[j] = on ? a.pad_s[q] : 0.0f;
+            pad.a[j] = on ? a.pad_a[q] : 0.0f;
+            pad.b[j] = on ? a.pad_b[q] : 0.0f;
         }
-
-        uint32_t t = a.t0;
-        uint4 aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
-        uint32_t abits = pick_word(aw, (t >> 5) & 3u) >> (t & 31u);
-        uint4 rw = philox(env, (t + 1u) >> 2, STREAM_RESET, p.key0, p.key1);
-        CartState rs = {uniform01_to(rw.x, p.reset_lo, p.reset_width), uniform01_to(rw.y, p.reset_lo, p.reset_width),
-                        uniform01_to(rw.z, p.reset_lo, p.reset_width), uniform01_to(rw.w, p.reset_lo, p.reset_width)};
-
-        float* obs = a.obs;
-        uint8_t* act_row = a.action;
-        float* rew_row = a.reward;
-        uint8_t* done_row = a.done;
-
-        for (uint32_t k = 0; k < a.K; ++k, ++t) {
-            if (k != 0u) {
-                if ((t & 127u) == 0u) aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
-                if ((t & 31u) == 0u) abits = pick_word(aw, (t >> 5) & 3u);
-                if (((t + 1u) & 3u) == 0u) {
-                    rw = philox(env, (t + 1u) >> 2, STREAM_RESET, p.key0, p.key1);
-                    rs.x = uniform01_to(rw.x, p.reset_lo, p.reset_width);
-                    rs.xd = uniform01_to(rw.y, p.reset_lo, p.reset_width);
-                    rs.th = uniform01_to(rw.z, p.reset_lo, p.reset_width);
-                    rs.thd = uniform01_to(rw.w, p.reset_lo, p.reset_width);
-                }
-            }
-            const uint32_t act = abits & 1u;
-            abits >>= 1;
-
-            const CartState nx = cartpole_step(p, s, act);
-#pragma unroll
-            for (int j = 0; j < W; ++j) ps[j] = __builtin_fmaf(pa[j], ps[j], act ? pb[j] : 0.0f);
-
-            const uint32_t len = ep + 1u;
-            const uint32_t term = crossed(p, nx);
-            const uint32_t trunc = (uint32_t)((p.max_steps != 0u) & (len >= p.max_steps));
-            const uint32_t d = term | (trunc << 1);
-
-            if (REC) {
-                *at(obs, off) = s.x;
-                *at(obs + plane, off) = s.xd;
-                *at(obs + 2 * plane, off) = s.th;
-                *at(obs + 3 * plane, off) = s.thd;
-                act_row[env] = (uint8_t)act;
-                *at(rew_row, off) = 1.0f;
-                done_row[env] = (uint8_t)d;
-                obs += 4 * plane;
-                act_row += a.n;
-                rew_row += a.n;
-                done_row += a.n;
-            }
-
-            const bool reset = d != 0u;
-            s.x = reset ? rs.x : nx.x;
-            s.xd = reset ? rs.xd : nx.xd;
-            s.th = reset ? rs.th : nx.th;
-            s.thd = reset ? rs.thd : nx.thd;
-            ep = reset ? 0u : len;
-#pragma unroll
-            for (int j = 0; j < W; ++j) ps[j] = reset ? 0.0f : ps[j];
-            if (STATS) {
-                n_eps += reset ? 1u : 0u;
-                n_len += reset ? len : 0u;
-                n_term += term;
-                n_trunc += trunc;
-            }
-        }
-
-        *at(c0, off) = s.x;
-        *at(c1, off) = s.xd;
-        *at(c2, off) = s.th;
-        *at(c3, off) = s.thd;
-        a.ep[env] = ep;
+        core.run(a.t0, a.K, pad);
+        core.store(a);
 #pragma unroll
         for (int j = 0; j < W; ++j)
-            if ((uint32_t)j < a.D) a.pad_s[(size_t)j * a.n + env] = ps[j];
+            if ((uint32_t)j < a.D) a.pad_s[(size_t)j * a.n + env] = pad.s[j];
     }
+    if (STATS) store_block_stats(a.stats, core.n_eps, core.n_len, core.n_term, core.n_trunc);
+}
 
-    if (STATS) {
-        __shared__ uint32_t part[kBlock / 64][4];
-        const uint32_t v0 = wave_sum(n_eps), v1 = wave_sum(n_len), v2 = wave_sum(n_term), v3 = wave_sum(n_trunc);
-        const uint32_t wave = threadIdx.x / 64u, lane = threadIdx.x % 64u;
-        if (lane == 0u) {
-            part[wave][0] = v0;
-            part[wave][1] = v1;
-            part[wave][2] = v2;
-            part[wave][3] = v3;
+// ---------------------------------------------------------------------------
+// Wide padding.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kChunk = 512;                 // steps per phase-1/phase-2 round
+constexpr uint32_t kChunkWords = kChunk / 32u;   // 32-bit bit words per env per round
+
+// Phase-1 hook: collects each step's action and done bits, 32 steps per word,
+// into this thread's LDS columns.
+struct BitRecorder {
+    uint32_t* lds_u;     // [kChunkWords][kBlock]
+    uint32_t* lds_d;
+    uint32_t col;        // threadIdx.x
+    uint32_t k = 0u;     // step index within the round
+    uint32_t ub = 0u, db = 0u;
+    __device__ __forceinline__ void operator()(uint32_t act, bool reset)
+    {
+        const uint32_t bit = k & 31u;
+        ub |= act << bit;
+        db |= (reset ? 1u : 0u) << bit;
+        if (bit == 31u) {
+            lds_u[(k >> 5) * kBlock + col] = ub;
+            lds_d[(k >> 5) * kBlock + col] = db;
+            ub = 0u;
+            db = 0u;
         }
-        __syncthreads();
-        if (threadIdx.x < 4u) {
-            uint32_t sum = 0u;
+        ++k;
+    }
+    __device__ __forceinline__ void flush()
+    {
+        if ((k & 31u) != 0u) {
+            lds_u[(k >> 5) * kBlock + col] = ub;
+            lds_d[(k >> 5) * kBlock + col] = db;
+        }
+    }
+};
+
+// Phase 2: G lanes per environment, W consecutive words per lane (W a multiple
+// of 4, loaded as float4).  Replays `steps` steps from the LDS bits for the
+// 64 / G environments a wave covers at a time, for all of the wave's 64 envs.
+template <int G, int W>
+__device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t* lds_u, const uint32_t* lds_d,
+                                               uint32_t steps)
+{
+    static_assert(W % 4 == 0 && 64 % G == 0, "bad wide-padding shape");
+    const uint32_t lane = threadIdx.x % 64u, wave = threadIdx.x / 64u;
+    const uint32_t gi = lane / G, gl = lane % G;            // env slot in the wave, lane in its group
+    const uint32_t chunk_words = (uint32_t)(G * W);
+    const uint32_t n_chunks = (a.Dp + chunk_words - 1u) / chunk_words;
+    // a pass covers 64 / G environments, so the wave's 64 take G passes
+    for (uint32_t pass = 0; pass < (uint32_t)G; ++pass) {
+        const uint32_t col = wave * 64u + pass * (64u / G) + gi;   // env column in the block
+        const uint32_t env = blockIdx.x * kBlock + col;
+        const bool live = env < a.n;
+        for (uint32_t c = 0; c < n_chunks; ++c) {
+            const uint32_t j0 = c * chunk_words + gl * W;          // first word of this lane
+            float s[W], pa[W], pb[W];
+            const size_t row = (size_t)env * a.Dp;
 #pragma unroll
-            for (int w = 0; w < kBlock / 64; ++w) sum += part[w][threadIdx.x];
-            a.stats[(size_t)blockIdx.x * 4u + threadIdx.x] = sum;
+            for (int i = 0; i < W; i += 4) {
+                const bool on = live && (j0 + i) < a.Dp;
+                const float4 vs = on ? *reinterpret_cast<const float4*>(a.pad_s + row + j0 + i) : float4{0, 0, 0, 0};
+                const float4 va = on ? *reinterpret_cast<const float4*>(a.pad_a + row + j0 + i) : float4{0, 0, 0, 0};
+                const float4 vb = on ? *reinterpret_cast<const float4*>(a.pad_b + row + j0 + i) : float4{0, 0, 0, 0};
+                s[i] = vs.x; s[i + 1] = vs.y; s[i + 2] = vs.z; s[i + 3] = vs.w;
+                pa[i] = va.x; pa[i + 1] = va.y; pa[i + 2] = va.z; pa[i + 3] = va.w;
+                pb[i] = vb.x; pb[i + 1] = vb.y; pb[i + 2] = vb.z; pb[i + 3] = vb.w;
+            }
+            for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
+                uint32_t ub = lds_u[w32 * kBlock + col];
+                uint32_t db = lds_d[w32 * kBlock + col];
+                const uint32_t m = min(32u, steps - w32 * 32u);
+                if (G == 64) {
+                    // one environment per wave: the bits are wave-uniform, so
+                    // each step is a scalar branch and one FMA per word
+                    ub = __builtin_amdgcn_readfirstlane(ub);
+                    db = __builtin_amdgcn_readfirstlane(db);
+                    for (uint32_t i = 0; i < m; ++i) {
+                        if ((ub >> i) & 1u) {
+#pragma unroll
+                            for (int j = 0; j < W; ++j) s[j] = __builtin_fmaf(pa[j], s[j], pb[j]);
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < W; ++j) s[j] = __builtin_fmaf(pa[j], s[j], 0.0f);
+                        }
+                        if ((db >> i) & 1u) {
+#pragma unroll
+                            for (int j = 0; j < W; ++j) s[j] = 0.0f;
+                        }
+                    }
+                } else {
+                    for (uint32_t i = 0; i < m; ++i) {
+                        const bool u = (ub >> i) & 1u;
+                        const bool d = (db >> i) & 1u;
+#pragma unroll
+                        for (int j = 0; j < W; ++j) {
+                            const float v = __builtin_fmaf(pa[j], s[j], u ? pb[j] : 0.0f);
+                            s[j] = d ? 0.0f : v;
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < W; i += 4) {
+                if (live && (j0 + i) < a.Dp)
+                    *reinterpret_cast<float4*>(a.pad_s + row + j0 + i) = float4{s[i], s[i + 1], s[i + 2], s[i + 3]};
+            }
         }
     }
 }
 
-// Initial state of every environment (episode beginning at step 0) and the
-// padding parameters, for the register (structure-of-arrays) padding layout.
+template <int G, int W, bool REC, bool STATS>
+__global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
+{
+    __shared__ uint32_t lds_u[kChunkWords * kBlock];
+    __shared__ uint32_t lds_d[kChunkWords * kBlock];
+    const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
+    const bool live = env < a.n;
+    CartCore<REC, STATS> core(a.p, env);
+    if (live) core.load(a);
+    for (uint32_t k0 = 0; k0 < a.K; k0 += kChunk) {
+        const uint32_t steps = min(kChunk, a.K - k0);
+        BitRecorder rec{lds_u, lds_d, threadIdx.x};
+        if (live) {
+            if (REC) core.set_rows(a, k0);
+            core.run(a.t0 + k0, steps, rec);
+            rec.flush();
+        }
+        __syncthreads();
+        replay_padding<G, W>(a, lds_u, lds_d, steps);
+        __syncthreads();
+    }
+    if (live) core.store(a);
+    if (STATS) store_block_stats(a.stats, core.n_eps, core.n_len, core.n_term, core.n_trunc);
+}
+
+// ---------------------------------------------------------------------------
+// Reset.
+// ---------------------------------------------------------------------------
+// Initial state of every environment (episode beginning at step 0).
 __global__ __launch_bounds__(kBlock) void k_reset_cart(DevParams p, uint32_t n, float* cart, uint32_t* ep)
 {
     const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
@@ -181,15 +413,15 @@ __global__ __launch_bounds__(kBlock) void k_reset_cart(DevParams p, uint32_t n, 
     ep[env] = 0u;
 }
 
-// Padding word j of env e lives at s[j * stride_j + e * stride_e]; one thread
-// per (word, env) pair, grid-strided over all D * n pairs.
+// Padding parameters and zero words: word j of env e lives at index
+// j * stride_j + e * stride_e; one thread per (word, env) pair, grid-strided.
 __global__ __launch_bounds__(kBlock) void k_reset_pad(DevParams p, uint32_t n, uint32_t D, size_t stride_j,
                                                       size_t stride_e, float a_lo, float a_width, float b_lo,
                                                       float b_width, float* s, float* pa, float* pb)
 {
     const size_t total = (size_t)n * D;
     for (size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x; i < total; i += (size_t)gridDim.x * kBlock) {
-        // env-fastest enumeration keeps both layouts' writes mostly contiguous
+        // consecutive threads take consecutive addresses in either layout
         const uint32_t env = (uint32_t)(stride_e == 1 ? i % n : i / D);
         const uint32_t j = (uint32_t)(stride_e == 1 ? i / n : i % D);
         const uint4 w = philox(env, j, STREAM_PARAMS, p.key0, p.key1);

@@ -27,7 +27,9 @@ struct rlsim {
     bool has_reset = false;
     float* cart = nullptr;      // [4][n]
     uint32_t* ep = nullptr;     // [n]
-    float* pad_s = nullptr;     // [D][n]
+    bool wide = false;          // padding layout: false [D][n], true [n][Dp]
+    uint32_t Dp = 0;            // wide row length (D rounded up to a multiple of 4)
+    float* pad_s = nullptr;
     float* pad_a = nullptr;
     float* pad_b = nullptr;
     std::string err;
@@ -127,21 +129,51 @@ void free_state(rlsim* h)
     h->pad_s = h->pad_a = h->pad_b = nullptr;
 }
 
+// Host-side layout conversion of the wide padding words, in 64 x 64 tiles:
+// rows[env * Dp + j] <-> planes[j * n + env].
+constexpr size_t kTile = 64;
+void transpose_rows_to_planes(const float* rows, float* planes, size_t n, size_t D, size_t Dp)
+{
+    for (size_t e0 = 0; e0 < n; e0 += kTile)
+        for (size_t j0 = 0; j0 < D; j0 += kTile)
+            for (size_t j = j0; j < std::min(D, j0 + kTile); ++j)
+                for (size_t e = e0; e < std::min(n, e0 + kTile); ++e) planes[j * n + e] = rows[e * Dp + j];
+}
+void transpose_planes_to_rows(const float* planes, float* rows, size_t n, size_t D, size_t Dp)
+{
+    for (size_t e0 = 0; e0 < n; e0 += kTile)
+        for (size_t j0 = 0; j0 < D; j0 += kTile)
+            for (size_t e = e0; e < std::min(n, e0 + kTile); ++e)
+                for (size_t j = j0; j < std::min(D, j0 + kTile); ++j) rows[e * Dp + j] = planes[j * n + e];
+}
+
 bool aligned4(const void* ptr) { return ((uintptr_t)ptr & 3u) == 0u; }
 
 unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 
-// Largest padding count of the register-resident (one thread per env) kernel.
+// Largest padding count of the register-resident (one thread per env) kernel;
+// above it the two-phase wide kernel holds the words.
 constexpr uint32_t kMaxRegisterWords = 16u;
 
 template <bool REC, bool STATS>
-hipError_t launch_cart(const StepArgs& a, hipStream_t s)
+hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
 {
     const dim3 grid(grid_for(a.n)), block(kBlock);
-    if (a.D == 0u) hipLaunchKernelGGL((k_cartpole_fused<0, REC, STATS>), grid, block, 0, s, a);
-    else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
-    else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
+    if (!wide) {
+        if (a.D == 0u) hipLaunchKernelGGL((k_cartpole_fused<0, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
+    } else {
+        // lanes per env x words per lane: 8 x 8 for up to 64 words (per-lane
+        // bits, 8 envs per wave); otherwise one env per wave with uniform bits
+        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<8, 8, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<64, 4, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<64, 8, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<64, 16, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<64, 32, REC, STATS>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_wide<64, 64, REC, STATS>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 
@@ -182,13 +214,13 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
     else rlsim_cfg_default(&c);
     if (const char* why = check_cfg(c)) return fail(nullptr, RLSIM_EINVAL, std::string("rlsim_create: ") + why);
     const uint32_t D = state_words - 4u;
-    if (D > kMaxRegisterWords)
-        return fail(nullptr, RLSIM_EUNSUPPORTED, "rlsim_create: more than 16 padding words not built yet");
 
     rlsim* h = new (std::nothrow) rlsim();
     if (!h) return fail(nullptr, RLSIM_ENOMEM, "rlsim_create: host allocation failed");
     h->n = n_envs;
     h->D = D;
+    h->wide = D > kMaxRegisterWords;
+    h->Dp = h->wide ? (D + 3u) & ~3u : D;
     h->cfg = c;
     h->stream = (hipStream_t)c.stream;
     hipError_t e = hipGetDevice(&h->device);
@@ -200,9 +232,14 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
     const size_t n = n_envs;
     e = hipMalloc(&h->cart, 4 * n * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&h->ep, n * sizeof(uint32_t));
-    if (e == hipSuccess && D) e = hipMalloc(&h->pad_s, (size_t)D * n * sizeof(float));
-    if (e == hipSuccess && D) e = hipMalloc(&h->pad_a, (size_t)D * n * sizeof(float));
-    if (e == hipSuccess && D) e = hipMalloc(&h->pad_b, (size_t)D * n * sizeof(float));
+    const size_t pad_bytes = (size_t)h->Dp * n * sizeof(float);
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_s, pad_bytes);
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_a, pad_bytes);
+    if (e == hipSuccess && D) e = hipMalloc(&h->pad_b, pad_bytes);
+    // the wide layout's row tails [D, Dp) stay zero for the handle's lifetime
+    if (e == hipSuccess && h->wide) e = hipMemset(h->pad_s, 0, pad_bytes);
+    if (e == hipSuccess && h->wide) e = hipMemset(h->pad_a, 0, pad_bytes);
+    if (e == hipSuccess && h->wide) e = hipMemset(h->pad_b, 0, pad_bytes);
     if (e != hipSuccess) {
         int rc = (e == hipErrorOutOfMemory) ? fail(nullptr, RLSIM_ENOMEM, "rlsim_create: device allocation failed")
                                             : hip_fail(nullptr, e, "rlsim_create: hipMalloc");
@@ -229,8 +266,10 @@ int rlsim_reset(rlsim_t* h, uint64_t seed)
         volatile float b_w = h->cfg.pad_b_high - h->cfg.pad_b_low;
         const size_t pairs = (size_t)h->n * h->D;
         const unsigned blocks = (unsigned)std::min<size_t>((pairs + kBlock - 1) / kBlock, 65536);
-        hipLaunchKernelGGL(k_reset_pad, dim3(blocks), dim3(kBlock), 0, h->stream, h->dp, h->n, h->D, (size_t)h->n,
-                           (size_t)1, h->cfg.pad_a_low, (float)a_w, h->cfg.pad_b_low, (float)b_w, h->pad_s,
+        const size_t stride_j = h->wide ? 1 : (size_t)h->n;
+        const size_t stride_e = h->wide ? (size_t)h->Dp : 1;
+        hipLaunchKernelGGL(k_reset_pad, dim3(blocks), dim3(kBlock), 0, h->stream, h->dp, h->n, h->D, stride_j,
+                           stride_e, h->cfg.pad_a_low, (float)a_w, h->cfg.pad_b_low, (float)b_w, h->pad_s,
                            h->pad_a, h->pad_b);
         e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(h, e, "rlsim_reset: launch");
@@ -263,6 +302,7 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     a.p = h->dp;
     a.n = h->n;
     a.D = h->D;
+    a.Dp = h->Dp;
     a.t0 = (uint32_t)h->t;
     a.K = K;
     a.cart = h->cart;
@@ -277,10 +317,10 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     a.stats = tr.block_stats;
     const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
     hipError_t e;
-    if (rec && stats) e = launch_cart<true, true>(a, h->stream);
-    else if (rec) e = launch_cart<true, false>(a, h->stream);
-    else if (stats) e = launch_cart<false, true>(a, h->stream);
-    else e = launch_cart<false, false>(a, h->stream);
+    if (rec && stats) e = launch_step<true, true>(a, h->wide, h->stream);
+    else if (rec) e = launch_step<true, false>(a, h->wide, h->stream);
+    else if (stats) e = launch_step<false, true>(a, h->wide, h->stream);
+    else e = launch_step<false, false>(a, h->wide, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");
     h->t += K;
     return RLSIM_OK;
@@ -293,16 +333,26 @@ int rlsim_get_state(rlsim_t* h, float* host_state, uint32_t* host_ep, uint64_t* 
     DeviceGuard g(h->device);
     if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_get_state: cannot select the handle's device");
     const size_t n = h->n;
+    std::vector<float> rows;     // wide layout staging, [n][Dp]
     hipError_t e = hipSuccess;
     if (host_state) {
         e = hipMemcpyAsync(host_state, h->cart, 4 * n * sizeof(float), hipMemcpyDeviceToHost, h->stream);
-        if (e == hipSuccess && h->D)
+        if (e == hipSuccess && h->D && !h->wide)
             e = hipMemcpyAsync(host_state + 4 * n, h->pad_s, (size_t)h->D * n * sizeof(float), hipMemcpyDeviceToHost,
                                h->stream);
+        if (e == hipSuccess && h->wide) {
+            try {
+                rows.resize((size_t)h->Dp * n);
+            } catch (const std::bad_alloc&) {
+                return fail(h, RLSIM_ENOMEM, "rlsim_get_state: host staging allocation failed");
+            }
+            e = hipMemcpyAsync(rows.data(), h->pad_s, rows.size() * sizeof(float), hipMemcpyDeviceToHost, h->stream);
+        }
     }
     if (e == hipSuccess && host_ep) e = hipMemcpyAsync(host_ep, h->ep, n * sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "rlsim_get_state");
+    if (host_state && h->wide) transpose_rows_to_planes(rows.data(), host_state + 4 * n, n, h->D, h->Dp);
     if (t_out) *t_out = h->t;
     return RLSIM_OK;
 }
@@ -315,12 +365,23 @@ int rlsim_set_state(rlsim_t* h, const float* host_state, const uint32_t* host_ep
     DeviceGuard g(h->device);
     if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_set_state: cannot select the handle's device");
     const size_t n = h->n;
+    std::vector<float> rows;
+    if (host_state && h->wide) {
+        try {
+            rows.assign((size_t)h->Dp * n, 0.0f);
+        } catch (const std::bad_alloc&) {
+            return fail(h, RLSIM_ENOMEM, "rlsim_set_state: host staging allocation failed");
+        }
+        transpose_planes_to_rows(host_state + 4 * n, rows.data(), n, h->D, h->Dp);
+    }
     hipError_t e = hipSuccess;
     if (host_state) {
         e = hipMemcpyAsync(h->cart, host_state, 4 * n * sizeof(float), hipMemcpyHostToDevice, h->stream);
-        if (e == hipSuccess && h->D)
+        if (e == hipSuccess && h->D && !h->wide)
             e = hipMemcpyAsync(h->pad_s, host_state + 4 * n, (size_t)h->D * n * sizeof(float), hipMemcpyHostToDevice,
                                h->stream);
+        if (e == hipSuccess && h->wide)
+            e = hipMemcpyAsync(h->pad_s, rows.data(), rows.size() * sizeof(float), hipMemcpyHostToDevice, h->stream);
     }
     if (e == hipSuccess && host_ep) e = hipMemcpyAsync(h->ep, host_ep, n * sizeof(uint32_t), hipMemcpyHostToDevice, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);

@@ -1,0 +1,90 @@
+"""GPU parity of the wide-padding kernels (the paper's state-size factor S).
+
+Beyond 16 padding words per environment the library switches to the two-phase
+kernel (cart-pole pass leaves action/done bits in LDS, then lane groups replay
+the padding recurrence with the words in registers).  Everything is compared
+bit for bit with the oracle: trajectory, block statistics, cart-pole state,
+all padding words and episode counters.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_helpers import assert_bit_equal, gpu_run, oracle_run
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2207_07736_amd  # noqa: F401
+
+
+# D values cover every kernel shape: 8x8 lane groups (<= 64 words), one env per
+# wave with 4/8/16/32/64 words per lane, ragged rows (D not a multiple of 4 or
+# of the chunk) and several word chunks per env (D > 4096).
+@pytest.mark.parametrize("D", [17, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
+def test_wide_padding_bit_exact(D):
+    n = 260                                   # two stats blocks, ragged tail
+    T = 140 if D > 1024 else 300
+    sched = [1, T - 1]
+    g = gpu_run(n, T, sched, D=D, seed=7)
+    r = oracle_run(n, T, sched, D=D, seed=7)
+    assert_bit_equal(g, r)
+    for a, b in zip(g["stats"], r["stats"]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("D", [64, 512])
+def test_wide_long_launch_crosses_chunks(D):
+    """K larger than the 512-step LDS round: the padding words are carried over
+    between rounds inside one launch."""
+    n, T = 300, 1100
+    g = gpu_run(n, T, [T], D=D, seed=workloads.PARITY_SEEDS[2])
+    r = oracle_run(n, T, [T], D=D, seed=workloads.PARITY_SEEDS[2])
+    assert_bit_equal(g, r)
+
+
+def test_wide_edge_configs():
+    cfg = workloads.cartpole(max_episode_steps=7, no_termination=1)
+    g = gpu_run(200, 60, [13, 47], D=70, seed=1, cfg=cfg)
+    r = oracle_run(200, 60, [13, 47], D=70, seed=1, cfg=cfg)
+    assert_bit_equal(g, r)
+
+
+def test_wide_set_state_round_trip():
+    from paper_2207_07736_amd import Simulator
+    n, D = 333, 130
+    sim = Simulator(n, D, workloads.CARTPOLE)
+    try:
+        sim.reset(3)
+        sim.step(20)
+        st, ep, t = sim.get_state()
+        rng = np.random.Generator(np.random.PCG64(0))
+        st2 = rng.standard_normal(st.shape).astype(np.float32)
+        sim.set_state(st2, ep, t)
+        back, ep2, t2 = sim.get_state()
+        assert np.array_equal(back.view(np.uint32), st2.view(np.uint32)) and np.array_equal(ep2, ep) and t2 == t
+    finally:
+        sim.close()
+
+
+@pytest.mark.parametrize("D", workloads.WORKLOADS["C4"]["D"])
+def test_c4_full_size_fused_equals_unfused(D):
+    """262,144 envs x 500 steps: one K=500 launch equals 500 K=1 launches bit for
+    bit (trajectory on sampled slices, the full final state), and the sampled
+    slices equal the oracle."""
+    w = workloads.WORKLOADS["C4"]
+    n, T = w["n"], w["T"]
+    slices = [(0, 256), (n - 256, n)]
+    fused = gpu_run(n, T, [T], D=D, seed=w["seed"], slices=slices)
+    unfused = gpu_run(n, T, [1] * T, D=D, seed=w["seed"], slices=slices)
+    assert_bit_equal(fused, unfused)
+    ref = [oracle_run(b - a, T, [T], D=D, seed=w["seed"], env0=a) for a, b in slices]
+    merged = {key: np.concatenate([x[key] for x in ref], axis=-1) for key in ("obs", "action", "reward", "done", "state")}
+    merged["ep"] = np.concatenate([x["ep"] for x in ref])
+    merged["t"] = T
+    assert_bit_equal(fused, merged)
