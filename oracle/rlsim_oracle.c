@@ -178,11 +178,13 @@ int orc_terminated(const orc_params* p, const float s[4])
 }
 
 /* Initial state of an episode that begins at global step t: stream RESET,  */
-/* counter block t/4, words 0..3 -> x, xd, th, thd.                          */
+/* counter block t/8, words 0..3 -> x, xd, th, thd.  Episodes of one env    */
+/* that begin in the same 8-step block would share a draw; with the default  */
+/* constants every episode lasts at least 8 steps, so none do.               */
 void orc_reset_draw(const orc_params* p, uint64_t seed, uint32_t env, uint32_t t, float out[4])
 {
     uint32_t w[4];
-    orc_draw(seed, env, t >> 2, ORC_STREAM_RESET, w);
+    orc_draw(seed, env, t >> 3, ORC_STREAM_RESET, w);
     for (int c = 0; c < 4; ++c) out[c] = orc_uniform(w[c], p->reset_low, p->reset_high);
 }
 
@@ -213,11 +215,12 @@ void orc_pad_params(const orc_params* p, uint64_t seed, uint32_t env, uint32_t j
     *b = orc_uniform(w[1], p->pad_b_low, p->pad_b_high);
 }
 
-/* One padding word: s <- a s + b u, rounded once (u is the action, 0 or 1). */
+/* One padding word: s <- a s + b u with u the action (0 or 1), rounded once:
+ * the fused a s + b when u = 1, the product a s when u = 0 (no b term). */
 float orc_pad_update(float s, float a, float b, int u)
 {
-    float bu = u ? b : 0.0f;
-    return fmaf(a, s, bu);
+    if (u) return fmaf(a, s, b);
+    return a * s;
 }
 
 /* ------------------------------------------------------------------------ */

@@ -21,6 +21,7 @@ struct DevParams {
     float thr_x, thr_th;  // +inf when termination is disabled
     uint32_t max_steps;   // 0 = no time limit
     float reset_lo, reset_width;   // width = reset_high - reset_low
+    float reset_width_u24;         // width * 2^-24 (exact; see uniform24_to)
     uint32_t key0, key1;  // Philox key: low and high word of the seed
 };
 
@@ -32,14 +33,18 @@ enum : uint32_t { STREAM_RESET = 0u, STREAM_ACTION = 1u, STREAM_PARAMS = 2u, STR
 // round's second product and the whole key schedule land on the scalar unit.
 __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t k0, uint32_t k1)
 {
+    // Recompute the key schedule at every call (scalar adds) rather than let
+    // it be hoisted into twenty loop-invariant scalars that spill to VGPR lanes.
+    asm volatile("" : "+s"(k0), "+s"(k1));
     uint32_t c3 = 0u;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         // full 64-bit products: one v_mad_u64_u32 gives both halves
         const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        // three-input XOR in one v_bitop3_b32 (truth table 0x96)
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
         c0 = n0;
         c1 = (uint32_t)p1;
         c2 = n2;
@@ -56,6 +61,13 @@ __device__ __forceinline__ float u24(uint32_t r) { return (float)(r >> 8) * 0x1.
 __device__ __forceinline__ float uniform01_to(uint32_t r, float lo, float width)
 {
     return __builtin_fmaf(u24(r), width, lo);
+}
+// The same value with the 2^-24 scale moved onto the width: (m 2^-24) w and
+// m (w 2^-24) are the same real number when w 2^-24 is exact, and the FMA
+// rounds it once either way.  width_u24 must equal width * 2^-24 exactly.
+__device__ __forceinline__ float uniform24_to(uint32_t r, float lo, float width_u24)
+{
+    return __builtin_fmaf((float)(r >> 8), width_u24, lo);
 }
 
 // Series sin / cos of degree 9 / 8, Horner form, one rounding per operation.
@@ -105,9 +117,11 @@ __device__ __forceinline__ CartState cartpole_step(const DevParams& p, const Car
 
 // Strict thresholds; NaN compares false.  Disabled termination is encoded as
 // infinite thresholds, under which every comparison is false.
+// |v| > t is the same predicate as (v < -t or v > t) for every v and t,
+// including signed zeros, infinities, NaN and negative t.
 __device__ __forceinline__ uint32_t crossed(const DevParams& p, const CartState& s)
 {
-    return (uint32_t)((s.x < -p.thr_x) | (s.x > p.thr_x) | (s.th < -p.thr_th) | (s.th > p.thr_th));
+    return (uint32_t)((__builtin_fabsf(s.x) > p.thr_x) | (__builtin_fabsf(s.th) > p.thr_th));
 }
 
 // Byte offset addressing: base + 32-bit unsigned offset lets the compiler use a

@@ -60,23 +60,29 @@ struct CartCore {
     uint32_t ep;
     uint4 aw;            // action words of the current 128-step block
     uint32_t abits;      // remaining action bits of the current 32-step word
-    CartState rs;        // reset draw for an episode beginning in the current 4-step block
+    CartState rs;        // reset draw for an episode beginning in the current 8-step block
     float* obs;          // trajectory row pointers (wave-uniform)
     uint8_t* act_row;
     float* rew_row;
     uint8_t* done_row;
     size_t plane;
-    uint32_t n_eps = 0u, n_len = 0u, n_term = 0u, n_trunc = 0u;
+    uint32_t ep_start = 0u;   // episode counter when the launch began
+    uint32_t n_eps = 0u, n_term = 0u, n_trunc = 0u;
 
     __device__ __forceinline__ CartCore(const DevParams& p_, uint32_t env_) : p(p_), env(env_) {}
+
+    // Sum of the lengths of the episodes that ended in this launch: every step
+    // adds one to the running episode, so the finished lengths plus the final
+    // running length equal the starting length plus K (mod 2^32).
+    __device__ __forceinline__ uint32_t finished_length_sum(uint32_t K) const { return ep_start + K - ep; }
 
     __device__ __forceinline__ void draw_reset(uint32_t block)
     {
         const uint4 w = philox(env, block, STREAM_RESET, p.key0, p.key1);
-        rs.x = uniform01_to(w.x, p.reset_lo, p.reset_width);
-        rs.xd = uniform01_to(w.y, p.reset_lo, p.reset_width);
-        rs.th = uniform01_to(w.z, p.reset_lo, p.reset_width);
-        rs.thd = uniform01_to(w.w, p.reset_lo, p.reset_width);
+        rs.x = uniform24_to(w.x, p.reset_lo, p.reset_width_u24);
+        rs.xd = uniform24_to(w.y, p.reset_lo, p.reset_width_u24);
+        rs.th = uniform24_to(w.z, p.reset_lo, p.reset_width_u24);
+        rs.thd = uniform24_to(w.w, p.reset_lo, p.reset_width_u24);
     }
 
     // Called before the step at t when t is a multiple of 32.
@@ -98,14 +104,14 @@ struct CartCore {
         const uint32_t trunc = (uint32_t)((p.max_steps != 0u) & (len >= p.max_steps));
         const uint32_t d = term | (trunc << 1);
         if (REC) {
-            const uint32_t o4 = opaque(env * 4u), o1 = opaque(env);
+            const uint32_t o4 = opaque(env * 4u);
             *at(obs, o4) = s.x;
             *at(obs + plane, o4) = s.xd;
             *at(obs + 2 * plane, o4) = s.th;
             *at(obs + 3 * plane, o4) = s.thd;
-            *at(act_row, o1) = (uint8_t)act;
+            *at(act_row, opaque(env)) = (uint8_t)act;
             *at(rew_row, o4) = 1.0f;
-            *at(done_row, o1) = (uint8_t)d;
+            *at(done_row, opaque(env)) = (uint8_t)d;
             obs += 4 * plane;
             act_row += plane;
             rew_row += plane;
@@ -120,51 +126,48 @@ struct CartCore {
         hook(act, reset);
         if (STATS) {
             n_eps += reset ? 1u : 0u;
-            n_len += reset ? len : 0u;
             n_term += term;
             n_trunc += trunc;
         }
     }
 
-    // Steps t0 .. t0+K-1.  The loop body covers the four steps that share one
-    // reset block ((t+1)/4 constant), so each reset draw is computed once, at a
-    // fixed place, and the body has no data-dependent control flow.
+    // Steps t0 .. t0+K-1.  The loop body covers the eight steps that share one
+    // reset block ((t+1)/8 constant), so each reset draw is computed once, at a
+    // fixed place, and the body has no data-dependent control flow.  A 32-step
+    // action word can only begin at the second step of a body (t+1 = 0 mod 8).
     template <class Hook>
     __device__ __forceinline__ void run(uint32_t t0, uint32_t K, Hook& hook)
     {
         uint32_t t = t0, k = 0;
         aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
         abits = pick_word(aw, (t >> 5) & 3u) >> (t & 31u);
-        if (((t + 1u) & 3u) != 0u) {
-            // up to three steps before the first block boundary; none of them
-            // starts a 32-step action word (they are not multiples of 4)
-            draw_reset((t + 1u) >> 2);
-            while (k < K && ((t + 1u) & 3u) != 0u) {
+        if (((t + 1u) & 7u) != 0u) {
+            // up to seven steps before the first block boundary; none of them
+            // but the first can start an action word (they are not multiples of 8)
+            draw_reset((t + 1u) >> 3);
+            while (k < K && ((t + 1u) & 7u) != 0u) {
                 step(hook);
                 ++t;
                 ++k;
             }
         }
-        // here t = 4m - 1: steps t .. t+3 draw resets from block m
-        for (; K - k >= 4u; k += 4u, t += 4u) {
-            draw_reset((t + 1u) >> 2);
+        // here t = 8m - 1: steps t .. t+7 draw resets from block m
+        for (; K - k >= 8u; k += 8u, t += 8u) {
+            draw_reset((t + 1u) >> 3);
             step(hook);
             if (((t + 1u) & 31u) == 0u) refresh_actions(t + 1u);
-            step(hook);
-            step(hook);
-            step(hook);
+            // a rolled loop: row pointers advance by one scalar add per step
+            // instead of eight precomputed per-step bases
+#pragma unroll 1
+            for (int i = 0; i < 7; ++i) step(hook);
         }
         if (k < K) {
-            draw_reset((t + 1u) >> 2);
+            draw_reset((t + 1u) >> 3);
             step(hook);
             ++t;
             ++k;
-            if (k < K) {
-                if ((t & 31u) == 0u) refresh_actions(t);
-                step(hook);
-                ++k;
-                if (k < K) step(hook);
-            }
+            if (k < K && (t & 31u) == 0u) refresh_actions(t);
+            for (; k < K; ++k) step(hook);
         }
     }
 
@@ -185,6 +188,7 @@ struct CartCore {
         s.th = a.cart[2 * pl + env];
         s.thd = a.cart[3 * pl + env];
         ep = a.ep[env];
+        ep_start = ep;
     }
 
     __device__ __forceinline__ void store(const StepArgs& a)
@@ -220,8 +224,16 @@ __device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t c0, 
     }
 }
 
-// Padding words held by one thread: s <- a s + (act ? b : +0), rounded once;
-// zeroed when the episode ends.
+// One padding word, s <- a s + b u rounded once: fma(a, s, b) when u = 1 and
+// the product a s when u = 0.  fma(a, s, -0) equals the product bit for bit
+// (x + -0 = x for every x, including both zeros), so a per-lane action costs
+// one select and one FMA per word.
+__device__ __forceinline__ float pad_update(float a, float s, float b, bool u)
+{
+    return __builtin_fmaf(a, s, u ? b : -0.0f);
+}
+
+// Padding words held by one thread; zeroed when the episode ends.
 template <int W>
 struct RegisterPad {
     float s[W > 0 ? W : 1], a[W > 0 ? W : 1], b[W > 0 ? W : 1];
@@ -229,14 +241,17 @@ struct RegisterPad {
     {
 #pragma unroll
         for (int j = 0; j < W; ++j) {
-            const float v = __builtin_fmaf(a[j], s[j], act ? b[j] : 0.0f);
+            const float v = pad_update(a[j], s[j], b[j], act != 0u);
             s[j] = reset ? 0.0f : v;
         }
     }
 };
 
+// Without padding words the kernel fits eight waves per SIMD (<= 64 VGPRs and
+// <= 96 SGPRs); asking for it keeps the register allocator inside that budget.
 template <int W, bool REC, bool STATS>
-__global__ __launch_bounds__(kBlock) void k_cartpole_fused(StepArgs a)
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(W == 0 ? 8 : 1)))
+void k_cartpole_fused(StepArgs a)
 {
     const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
     CartCore<REC, STATS> core(a.p, env);
@@ -258,7 +273,10 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_fused(StepArgs a)
         for (int j = 0; j < W; ++j)
             if ((uint32_t)j < a.D) a.pad_s[(size_t)j * a.n + env] = pad.s[j];
     }
-    if (STATS) store_block_stats(a.stats, core.n_eps, core.n_len, core.n_term, core.n_trunc);
+    if (STATS) {
+        const uint32_t len_sum = env < a.n ? core.finished_length_sum(a.K) : 0u;
+        store_block_stats(a.stats, core.n_eps, len_sum, core.n_term, core.n_trunc);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -343,7 +361,7 @@ __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t
                             for (int j = 0; j < W; ++j) s[j] = __builtin_fmaf(pa[j], s[j], pb[j]);
                         } else {
 #pragma unroll
-                            for (int j = 0; j < W; ++j) s[j] = __builtin_fmaf(pa[j], s[j], 0.0f);
+                            for (int j = 0; j < W; ++j) s[j] = pa[j] * s[j];
                         }
                         if ((db >> i) & 1u) {
 #pragma unroll
@@ -356,7 +374,7 @@ __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t
                         const bool d = (db >> i) & 1u;
 #pragma unroll
                         for (int j = 0; j < W; ++j) {
-                            const float v = __builtin_fmaf(pa[j], s[j], u ? pb[j] : 0.0f);
+                            const float v = pad_update(pa[j], s[j], pb[j], u);
                             s[j] = d ? 0.0f : v;
                         }
                     }
@@ -393,7 +411,10 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
         __syncthreads();
     }
     if (live) core.store(a);
-    if (STATS) store_block_stats(a.stats, core.n_eps, core.n_len, core.n_term, core.n_trunc);
+    if (STATS) {
+        const uint32_t len_sum = live ? core.finished_length_sum(a.K) : 0u;
+        store_block_stats(a.stats, core.n_eps, len_sum, core.n_term, core.n_trunc);
+    }
 }
 
 // ---------------------------------------------------------------------------

@@ -96,6 +96,7 @@ DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
     p.max_steps = c.max_episode_steps;
     p.reset_lo = c.reset_low;
     p.reset_width = width;
+    p.reset_width_u24 = std::ldexp((float)width, -24);   // exact: check_cfg bounds the width
     p.key0 = (uint32_t)(seed & 0xFFFFFFFFull);
     p.key1 = (uint32_t)(seed >> 32);
     return p;
@@ -112,6 +113,12 @@ const char* check_cfg(const rlsim_cfg& c)
     if (!(c.half_length > 0.0f)) return "cfg: half_length must be positive";
     if (!(c.tau > 0.0f)) return "cfg: tau must be positive";
     if (c.reset_low > c.reset_high) return "cfg: reset_low > reset_high";
+    {
+        // the kernels scale the reset width by 2^-24, which must stay exact
+        volatile float width = c.reset_high - c.reset_low;
+        if (!std::isfinite((float)width)) return "cfg: reset range too wide";
+        if (width != 0.0f && std::fabs((float)width) < 0x1.0p-100f) return "cfg: reset range narrower than 2^-100";
+    }
     if (c.pad_a_low > c.pad_a_high || c.pad_b_low > c.pad_b_high) return "cfg: padding range low > high";
     if ((c.flags & ~(uint32_t)RLSIM_F_NO_TERMINATION) != 0u) return "cfg: unknown flag bits";
     return nullptr;

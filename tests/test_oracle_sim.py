@@ -245,3 +245,24 @@ def test_padding_closed_form_random_actions():
                 assert abs(float(st[4 + j, e]) - float(exact)) <= bound, (e, j)
                 if t0 == T:
                     assert st[4 + j, e] == 0
+
+
+def test_episodes_last_at_least_eight_steps():
+    """With the default constants no episode ends within 7 steps: from every
+    point of a grid over the initial-state box (corners included) and under all
+    2^7 action sequences the post-step state stays inside the thresholds for 7
+    steps.  So two episodes of one environment never begin in the same 8-step
+    block and never share a reset draw."""
+    import itertools
+    grid = np.linspace(-0.05, 0.05, 3, dtype=np.float32)
+    for st in itertools.product(grid, repeat=4):
+        for acts in itertools.product((0, 1), repeat=7):
+            s = np.array(st, dtype=np.float32)
+            for a in acts:
+                s = oracle.cartpole_step(P, s, a)
+                assert not oracle.terminated(P, s), (st, acts)
+    # and 8 steps can suffice: the fastest fall from a corner ends at step 8
+    s = np.array([0.0, 0.05, 0.05, 0.05], dtype=np.float32)
+    for _ in range(7):
+        s = oracle.cartpole_step(P, s, 0)
+    assert oracle.terminated(P, oracle.cartpole_step(P, s, 0))
