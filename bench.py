@@ -26,7 +26,11 @@ import workloads  # noqa: E402
 
 METRIC = "env-steps/sec at 1 MI355X; achieved HBM GB/s vs peak; fused/unfused speedup"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+COPY_BYTES = 1 << 30        # size of the plain copy used to calibrate the HBM byte counters
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"hbm_traffic__{workload}.txt")
 
 
 def kernel_source_digest() -> str:
@@ -40,17 +44,78 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+def _read_kv(path: str) -> dict:
+    out = {}
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#") and ":" in line:
+                k, v = line.split(":", 1)
+                out[k.strip()] = v.strip()
+    return out
+
+
 def stored_traffic(workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or None."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when there is none or the kernel sources changed since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as f:
-            d = json.load(f)
-    except (OSError, ValueError):
+        d = _read_kv(traffic_file(workload))
+    except OSError:
         return None
-    e = d.get(workload)
-    if not e or e.get("source_digest") != kernel_source_digest():
+    if d.get("source_digest") != kernel_source_digest():
         return None
-    return float(e["hbm_bytes_per_launch"])
+    return float(d["hbm_bytes_per_launch"])
+
+
+def ingest_pmc(fetch_csv: str, write_csv: str, workload: str, kernel_prefix: str) -> str:
+    """Turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, then WRITE_SIZE, KiB per
+    dispatch) into the traffic summary: each counter is scaled by what it reads
+    for the plain device copy of COPY_BYTES that --copy-calibration runs."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    f, w = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    kf = [k for k in f if k.startswith(kernel_prefix)]
+    copy_f = [k for k in f if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy_w = [k for k in w if "copy" in k.lower() or "elementwise" in k.lower()]
+    if len(kf) != 1 or not copy_f or not copy_w:
+        raise SystemExit(f"cannot find the kernel / copy dispatches: {list(f)}")
+    k = kf[0]
+    fetch_kib = statistics.median(f[k])
+    write_kib = statistics.median(w[k])
+    # the copy reads and writes COPY_BYTES; its dispatch is the largest such one
+    cf = max(max(v) for kk, v in f.items() if kk in copy_f)
+    cw = max(max(v) for kk, v in w.items() if kk in copy_w)
+    fetch_scale = COPY_BYTES / (cf * 1024.0)
+    write_scale = COPY_BYTES / (cw * 1024.0)
+    hbm = fetch_kib * 1024.0 * fetch_scale + write_kib * 1024.0 * write_scale
+    path = traffic_file(workload)
+    with open(path, "w") as fh:
+        fh.write(f"""# HBM traffic of one launch, from rocprofv3 counters (KiB per dispatch, median)
+# commands (repository root on the GPU box, run from /tmp with TMPDIR=/tmp):
+#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/pmc_fetch -o f -- python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu --no-sweep --no-unfused --copy-calibration
+#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/pmc_write -o w -- python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu --no-sweep --no-unfused --copy-calibration
+#   python bench.py --ingest-pmc <out>/pmc_fetch/f_counter_collection.csv <out>/pmc_write/w_counter_collection.csv
+# counters are scaled by what they read for a plain {COPY_BYTES} B device copy (torch copy_)
+kernel: {k}
+workload: {workload}
+source_digest: {kernel_source_digest()}
+fetch_kib_per_dispatch: {fetch_kib:.1f}
+write_kib_per_dispatch: {write_kib:.1f}
+copy_fetch_kib: {cf:.1f}
+copy_write_kib: {cw:.1f}
+copy_fetch_scale: {fetch_scale:.4f}
+copy_write_scale: {write_scale:.4f}
+hbm_bytes_per_launch: {hbm:.0f}
+""")
+    return path
 
 
 def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
@@ -146,13 +211,22 @@ def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-unfused", action="store_true", help="skip the K=1 contrast")
     ap.add_argument("--no-sweep", action="store_true", help="skip the K and state-size sweeps")
     ap.add_argument("--cpu-slice-envs", type=int, default=65536)
     ap.add_argument("--cpu-slices", type=int, default=8)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain device copy of 1 GiB (HBM counter calibration)")
+    ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the HBM traffic summary from two rocprofv3 counter CSVs and exit")
     args = ap.parse_args()
+
+    if args.ingest_pmc:
+        w = workloads.WORKLOADS["C3"]
+        print(ingest_pmc(args.ingest_pmc[0], args.ingest_pmc[1], w["name"], "void rlsim_dev::k_cartpole_fused<0"))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the environments shard by range with no "
@@ -244,6 +318,14 @@ def main() -> int:
 
     del traj
     sim.close()
+
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     if not args.no_sweep:
         result["sweeps"] = fusion_sweeps(stream)

@@ -17,7 +17,6 @@ struct DevParams {
     float inv_total;      // 1 / (masscart + masspole)
     float m_over_M;       // masspole * inv_total
     float ml_over_M;      // pole_ml * inv_total
-    float four_thirds;    // 4 / 3
     float thr_x, thr_th;  // +inf when termination is disabled
     uint32_t max_steps;   // 0 = no time limit
     float reset_lo, reset_width;   // width = reset_high - reset_low
@@ -104,7 +103,7 @@ __device__ __forceinline__ CartState cartpole_step(const DevParams& p, const Car
     const float ml_thd2 = p.pole_ml * (s.thd * s.thd);
     const float temp = __builtin_fmaf(ml_thd2, sn, force) * p.inv_total;
     const float num = __builtin_fmaf(-cs, temp, p.gravity * sn);
-    const float den = p.half_length * __builtin_fmaf(-p.m_over_M, cs * cs, p.four_thirds);
+    const float den = p.half_length * __builtin_fmaf(-p.m_over_M, cs * cs, 4.0f / 3.0f);
     const float thacc = num / den;                       // IEEE division
     const float xacc = __builtin_fmaf(-(p.ml_over_M * thacc), cs, temp);
     CartState o;
@@ -119,9 +118,9 @@ __device__ __forceinline__ CartState cartpole_step(const DevParams& p, const Car
 // infinite thresholds, under which every comparison is false.
 // |v| > t is the same predicate as (v < -t or v > t) for every v and t,
 // including signed zeros, infinities, NaN and negative t.
-__device__ __forceinline__ uint32_t crossed(const DevParams& p, const CartState& s)
+__device__ __forceinline__ bool crossed(const DevParams& p, const CartState& s)
 {
-    return (uint32_t)((__builtin_fabsf(s.x) > p.thr_x) | (__builtin_fabsf(s.th) > p.thr_th));
+    return (__builtin_fabsf(s.x) > p.thr_x) || (__builtin_fabsf(s.th) > p.thr_th);
 }
 
 // Byte offset addressing: base + 32-bit unsigned offset lets the compiler use a

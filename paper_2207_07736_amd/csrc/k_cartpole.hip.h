@@ -42,13 +42,14 @@ __device__ __forceinline__ uint32_t pick_word(const uint4& w, uint32_t q)
     return q == 0u ? w.x : q == 1u ? w.y : q == 2u ? w.z : w.w;
 }
 
-// Hides a per-lane 32-bit offset from loop strength reduction, so that a store
-// is addressed as (scalar 64-bit row base) + (per-lane 32-bit offset) rather
-// than through a per-lane 64-bit pointer advanced every step.
-__device__ __forceinline__ uint32_t opaque(uint32_t v)
+// Workgroups are dispatched to the 8 XCDs round-robin (hardware block b runs
+// on XCD b mod 8).  This bijection hands XCD x the contiguous logical blocks
+// [x per, (x+1) per), so each XCD's L2 and TLB see one contiguous slice of
+// every trajectory row instead of a 1-in-8 comb across all of it.
+__device__ __forceinline__ uint32_t xcd_block()
 {
-    asm volatile("" : "+v"(v));
-    return v;
+    const uint32_t nb = gridDim.x, b = blockIdx.x, per = nb / 8u;
+    return b < per * 8u ? (b % 8u) * per + b / 8u : b;
 }
 
 // One environment's cart-pole state and RNG words, advanced step by step.
@@ -67,9 +68,11 @@ struct CartCore {
     uint8_t* done_row;
     size_t plane;
     uint32_t ep_start = 0u;   // episode counter when the launch began
+    uint32_t off4, off1a, off1d;   // per-lane byte offsets of this env in a row
     uint32_t n_eps = 0u, n_term = 0u, n_trunc = 0u;
 
-    __device__ __forceinline__ CartCore(const DevParams& p_, uint32_t env_) : p(p_), env(env_) {}
+    __device__ __forceinline__ CartCore(const DevParams& p_, uint32_t env_)
+        : p(p_), env(env_), off4(env_ * 4u), off1a(env_), off1d(env_) {}
 
     // Sum of the lengths of the episodes that ended in this launch: every step
     // adds one to the running episode, so the finished lengths plus the final
@@ -100,24 +103,25 @@ struct CartCore {
         abits >>= 1;
         const CartState nx = cartpole_step(p, s, act);
         const uint32_t len = ep + 1u;
-        const uint32_t term = crossed(p, nx);
-        const uint32_t trunc = (uint32_t)((p.max_steps != 0u) & (len >= p.max_steps));
-        const uint32_t d = term | (trunc << 1);
+        const bool term = crossed(p, nx);
+        const bool trunc = (p.max_steps != 0u) && (len >= p.max_steps);
+        const uint32_t d = (trunc ? 2u : 0u) + (uint32_t)term;
         if (REC) {
-            const uint32_t o4 = opaque(env * 4u);
-            *at(obs, o4) = s.x;
-            *at(obs + plane, o4) = s.xd;
-            *at(obs + 2 * plane, o4) = s.th;
-            *at(obs + 3 * plane, o4) = s.thd;
-            *at(act_row, opaque(env)) = (uint8_t)act;
-            *at(rew_row, o4) = 1.0f;
-            *at(done_row, opaque(env)) = (uint8_t)d;
+            // the offsets are passed through an empty asm in place each step
+            asm volatile("" : "+v"(off4), "+v"(off1a), "+v"(off1d));
+            *at(obs, off4) = s.x;
+            *at(obs + plane, off4) = s.xd;
+            *at(obs + 2 * plane, off4) = s.th;
+            *at(obs + 3 * plane, off4) = s.thd;
+            *at(act_row, off1a) = (uint8_t)act;
+            *at(rew_row, off4) = 1.0f;
+            *at(done_row, off1d) = (uint8_t)d;
             obs += 4 * plane;
             act_row += plane;
             rew_row += plane;
             done_row += plane;
         }
-        const bool reset = d != 0u;
+        const bool reset = term || trunc;
         s.x = reset ? rs.x : nx.x;
         s.xd = reset ? rs.xd : nx.xd;
         s.th = reset ? rs.th : nx.th;
@@ -126,8 +130,8 @@ struct CartCore {
         hook(act, reset);
         if (STATS) {
             n_eps += reset ? 1u : 0u;
-            n_term += term;
-            n_trunc += trunc;
+            n_term += term ? 1u : 0u;
+            n_trunc += trunc ? 1u : 0u;
         }
     }
 
@@ -204,7 +208,8 @@ struct CartCore {
 
 // Sums the four episode counters over the workgroup and writes one row of the
 // block statistics (all threads of the block must call this).
-__device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3)
+__device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t blk, uint32_t c0, uint32_t c1, uint32_t c2,
+                                                  uint32_t c3)
 {
     __shared__ uint32_t part[kBlock / 64][4];
     const uint32_t v0 = wave_sum(c0), v1 = wave_sum(c1), v2 = wave_sum(c2), v3 = wave_sum(c3);
@@ -220,7 +225,7 @@ __device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t c0, 
         uint32_t sum = 0u;
 #pragma unroll
         for (int w = 0; w < kBlock / 64; ++w) sum += part[w][threadIdx.x];
-        stats[(size_t)blockIdx.x * 4u + threadIdx.x] = sum;
+        stats[(size_t)blk * 4u + threadIdx.x] = sum;
     }
 }
 
@@ -253,7 +258,8 @@ template <int W, bool REC, bool STATS>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(W == 0 ? 8 : 1)))
 void k_cartpole_fused(StepArgs a)
 {
-    const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
+    const uint32_t blk = xcd_block();
+    const uint32_t env = blk * kBlock + threadIdx.x;
     CartCore<REC, STATS> core(a.p, env);
     if (env < a.n) {
         core.load(a);
@@ -275,7 +281,7 @@ void k_cartpole_fused(StepArgs a)
     }
     if (STATS) {
         const uint32_t len_sum = env < a.n ? core.finished_length_sum(a.K) : 0u;
-        store_block_stats(a.stats, core.n_eps, len_sum, core.n_term, core.n_trunc);
+        store_block_stats(a.stats, blk, core.n_eps, len_sum, core.n_term, core.n_trunc);
     }
 }
 
@@ -320,7 +326,7 @@ struct BitRecorder {
 // 64 / G environments a wave covers at a time, for all of the wave's 64 envs.
 template <int G, int W>
 __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t* lds_u, const uint32_t* lds_d,
-                                               uint32_t steps)
+                                               uint32_t steps, uint32_t blk)
 {
     static_assert(W % 4 == 0 && 64 % G == 0, "bad wide-padding shape");
     const uint32_t lane = threadIdx.x % 64u, wave = threadIdx.x / 64u;
@@ -330,7 +336,7 @@ __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t
     // a pass covers 64 / G environments, so the wave's 64 take G passes
     for (uint32_t pass = 0; pass < (uint32_t)G; ++pass) {
         const uint32_t col = wave * 64u + pass * (64u / G) + gi;   // env column in the block
-        const uint32_t env = blockIdx.x * kBlock + col;
+        const uint32_t env = blk * kBlock + col;
         const bool live = env < a.n;
         for (uint32_t c = 0; c < n_chunks; ++c) {
             const uint32_t j0 = c * chunk_words + gl * W;          // first word of this lane
@@ -394,7 +400,8 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
 {
     __shared__ uint32_t lds_u[kChunkWords * kBlock];
     __shared__ uint32_t lds_d[kChunkWords * kBlock];
-    const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
+    const uint32_t blk = xcd_block();
+    const uint32_t env = blk * kBlock + threadIdx.x;
     const bool live = env < a.n;
     CartCore<REC, STATS> core(a.p, env);
     if (live) core.load(a);
@@ -407,13 +414,13 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
             rec.flush();
         }
         __syncthreads();
-        replay_padding<G, W>(a, lds_u, lds_d, steps);
+        replay_padding<G, W>(a, lds_u, lds_d, steps, blk);
         __syncthreads();
     }
     if (live) core.store(a);
     if (STATS) {
         const uint32_t len_sum = live ? core.finished_length_sum(a.K) : 0u;
-        store_block_stats(a.stats, core.n_eps, len_sum, core.n_term, core.n_trunc);
+        store_block_stats(a.stats, blk, core.n_eps, len_sum, core.n_term, core.n_trunc);
     }
 }
 

@@ -79,7 +79,6 @@ DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
     volatile float inv_total = 1.0f / total;
     volatile float m_over_M = c.masspole * inv_total;
     volatile float ml_over_M = pole_ml * inv_total;
-    volatile float four_thirds = 4.0f / 3.0f;
     volatile float width = c.reset_high - c.reset_low;
     p.gravity = c.gravity;
     p.force_mag = c.force_mag;
@@ -89,7 +88,6 @@ DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
     p.inv_total = inv_total;
     p.m_over_M = m_over_M;
     p.ml_over_M = ml_over_M;
-    p.four_thirds = four_thirds;
     const bool noterm = (c.flags & RLSIM_F_NO_TERMINATION) != 0u;
     p.thr_x = noterm ? INFINITY : c.x_threshold;
     p.thr_th = noterm ? INFINITY : c.theta_threshold_rad;
