@@ -95,12 +95,30 @@ struct CartCore {
         abits = pick_word(aw, (t >> 5) & 3u);
     }
 
-    // Step t.  hook(act, reset) sees the action and whether the episode ended.
+    // Step t with the random action of the current action word.
     template <class Hook>
     __device__ __forceinline__ void step(Hook& hook)
     {
         const uint32_t act = abits & 1u;
         abits >>= 1;
+        step_with(act, hook);
+        if (REC) advance_rows();
+    }
+
+    __device__ __forceinline__ void advance_rows()
+    {
+        obs += 4 * plane;
+        act_row += plane;
+        rew_row += plane;
+        done_row += plane;
+    }
+
+    // One step with the given action: record the row, Euler-step, terminate /
+    // truncate, auto-reset.  hook(act, reset) sees the action and whether the
+    // episode ended.  The row pointers are left for the caller to advance.
+    template <class Hook>
+    __device__ __forceinline__ void step_with(uint32_t act, Hook& hook)
+    {
         const CartState nx = cartpole_step(p, s, act);
         const uint32_t len = ep + 1u;
         const bool term = crossed(p, nx);
@@ -116,10 +134,6 @@ struct CartCore {
             *at(act_row, off1a) = (uint8_t)act;
             *at(rew_row, off4) = 1.0f;
             *at(done_row, off1d) = (uint8_t)d;
-            obs += 4 * plane;
-            act_row += plane;
-            rew_row += plane;
-            done_row += plane;
         }
         const bool reset = term || trunc;
         s.x = reset ? rs.x : nx.x;
@@ -237,6 +251,10 @@ __device__ __forceinline__ float pad_update(float a, float s, float b, bool u)
 {
     return __builtin_fmaf(a, s, u ? b : -0.0f);
 }
+
+struct NoPad {
+    __device__ __forceinline__ void operator()(uint32_t, bool) {}
+};
 
 // Padding words held by one thread; zeroed when the episode ends.
 template <int W>

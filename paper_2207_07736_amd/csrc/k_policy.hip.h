@@ -1,0 +1,312 @@
+// k_policy.hip.h -- the simulation/inference loop with an on-device MLP policy
+// fused into the K-step kernel (the paper's Future Work: simulation/inference
+// fusion).  Per step every environment evaluates
+//     h1 = tanh(W1 obs + b1), h2 = tanh(W2 h1 + b2), logits = W3 h2 + b3,
+//     p0 = softmax(logits)[0] = 1 / (1 + exp(l1 - l0)),
+// samples action 0 when u < p0 (u from Philox stream POLICY), then takes the
+// cart-pole step exactly as the random-action kernel does.
+//
+// Matrix layout.  A wave owns 64 environments (lane = environment for the
+// cart-pole state) and runs the MLP as two 32-environment column tiles of the
+// transposed product  Z^T = W * H^T  (weights = MFMA A operand, activations =
+// B operand, environments = N).  With the 32x32 MFMA accumulator layout (lane l,
+// register i holds row 8(i/4) + 4(l/32) + (i%4) of column l%32) each lane
+// already holds the values the next layer's B operand needs from it, provided
+// the next layer's K index runs over hidden units in that order; the weights are
+// gathered in that permuted order once per launch, so activations never move
+// between lanes.  The output layer puts logit rows at 0,1 (tile 0) and 4,5
+// (tile 1) so that every lane finds its own environment's logits in its own
+// registers 0 and 1.
+#pragma once
+
+#include "k_cartpole.hip.h"
+
+namespace rlsim_dev {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct PolicyArgs {
+    const void* w1;     // [64][4]  f32 or bf16 bits
+    const float* b1;    // [64] or null
+    const void* w2;     // [64][64]
+    const float* b2;    // [64] or null
+    const void* w3;     // [2][64]
+    const float* b3;    // [2] or null
+    float* p0;          // [K][n] or null
+};
+
+// Hidden unit held by accumulator register i of a lane in half h (0: lanes
+// 0-31, 1: lanes 32-63) of row tile M.
+__device__ __forceinline__ uint32_t acc_row(uint32_t M, uint32_t i, uint32_t h)
+{
+    return 32u * M + 8u * (i / 4u) + 4u * h + (i % 4u);
+}
+
+__device__ __forceinline__ float tanh_fast(float x)
+{
+    // tanh x = 1 - 2 / (1 + e^(2x)); e^(2x) = 2^(2 x log2 e) on the exp2 unit
+    const float e = __builtin_amdgcn_exp2f(x * 2.88539008177792681472f);
+    return __builtin_fmaf(-2.0f, __builtin_amdgcn_rcpf(1.0f + e), 1.0f);
+}
+
+__device__ __forceinline__ float weight_at(const void* w, bool bf16, uint32_t idx)
+{
+    if (bf16) {
+        const uint16_t bits = reinterpret_cast<const uint16_t*>(w)[idx];
+        return __uint_as_float((uint32_t)bits << 16);
+    }
+    return reinterpret_cast<const float*>(w)[idx];
+}
+
+__device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
+
+// Per-lane accumulator initialisation with the biases of row tile M.
+__device__ __forceinline__ floatx16 bias_tile(const float* lds_b, uint32_t M, uint32_t h)
+{
+    floatx16 c;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) c[i] = lds_b[acc_row(M, (uint32_t)i, h)];
+    return c;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MLP: all three layers on v_mfma_f32_32x32x16_bf16.
+// ---------------------------------------------------------------------------
+struct MlpBf16 {
+    bf16x8 a1[2];        // layer 1, row tiles 0/1; K = obs in k 0-3 and 8-11
+    bf16x8 a2[2][4];     // layer 2, [out tile][K step]
+    bf16x8 a3[4];        // layer 3, [K step]; rows 0,1 and 4,5 = the two logits
+    float b3_0, b3_1;
+
+    // hidden-input unit of K step s, element j, for a lane in half h
+    __device__ static uint32_t k_unit(uint32_t s, uint32_t j, uint32_t h)
+    {
+        return acc_row(s / 2u, 8u * (s % 2u) + j, h);
+    }
+
+    __device__ void load(const PolicyArgs& w, uint32_t lane)
+    {
+        const uint32_t h = lane / 32u, col = lane % 32u;
+#pragma unroll
+        for (int M = 0; M < 2; ++M)
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                a1[M][j] = to_bf16(j < 4 ? weight_at(w.w1, true, (32u * M + col) * 4u + j) : 0.0f);
+#pragma unroll
+        for (int Mo = 0; Mo < 2; ++Mo)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    a2[Mo][s][j] = to_bf16(weight_at(w.w2, true, (32u * Mo + col) * 64u + k_unit(s, j, h)));
+        const int out = (col == 0u || col == 4u) ? 0 : (col == 1u || col == 5u) ? 1 : -1;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                a3[s][j] = to_bf16(out >= 0 ? weight_at(w.w3, true, (uint32_t)out * 64u + k_unit(s, j, h)) : 0.0f);
+        b3_0 = w.b3 ? w.b3[0] : 0.0f;
+        b3_1 = w.b3 ? w.b3[1] : 0.0f;
+    }
+
+    // p0 of this lane's environment; obs is this lane's pre-step state.
+    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, uint32_t lane) const
+    {
+        const uint32_t h = lane / 32u;
+        const bf16x8 zero8 = {};
+        bf16x8 own = zero8;
+        own[0] = to_bf16(obs.x);
+        own[1] = to_bf16(obs.xd);
+        own[2] = to_bf16(obs.th);
+        own[3] = to_bf16(obs.thd);
+        float l0 = 0.0f, l1 = 0.0f;
+#pragma unroll
+        for (uint32_t T = 0; T < 2u; ++T) {
+            // layer 1: tile T's environments live in half T
+            const bf16x8 bin = (h == T) ? own : zero8;
+            floatx16 c1[2];
+#pragma unroll
+            for (int M = 0; M < 2; ++M)
+                c1[M] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[M], bin, bias_tile(lds_b1, M, h), 0, 0, 0);
+            bf16x8 b1[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) b1[s][j] = to_bf16(tanh_fast(c1[s / 2][8 * (s % 2) + j]));
+            // layer 2
+            floatx16 c2[2];
+#pragma unroll
+            for (int Mo = 0; Mo < 2; ++Mo) {
+                c2[Mo] = bias_tile(lds_b2, Mo, h);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[Mo][s], b1[s], c2[Mo], 0, 0, 0);
+            }
+            bf16x8 b2[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) b2[s][j] = to_bf16(tanh_fast(c2[s / 2][8 * (s % 2) + j]));
+            // layer 3: rows 0,1 (tile 0) / 4,5 (tile 1) are registers 0,1 of the owning half
+            floatx16 c3 = {};
+            c3[0] = b3_0;
+            c3[1] = b3_1;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[s], b2[s], c3, 0, 0, 0);
+            if (h == T) {
+                l0 = c3[0];
+                l1 = c3[1];
+            }
+        }
+        // softmax over two logits
+        const float e = __builtin_amdgcn_exp2f((l1 - l0) * 1.44269504088896340736f);
+        return __builtin_amdgcn_rcpf(1.0f + e);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// fp32 MLP: layers 1 and 2 on v_mfma_f32_32x32x2_f32, layer 3 on the VALU.
+// ---------------------------------------------------------------------------
+struct MlpF32 {
+    float a1[2][4];      // layer 1 [row tile][obs index]; both halves hold the same weight
+    float a2[2][2][16];  // layer 2 [out tile][in tile][accumulator register]
+    float w3[2][2][16];  // layer 3 [logit][in tile][accumulator register]
+    float b3_0, b3_1;
+
+    __device__ void load(const PolicyArgs& w, uint32_t lane)
+    {
+        const uint32_t h = lane / 32u, col = lane % 32u;
+#pragma unroll
+        for (int M = 0; M < 2; ++M)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) a1[M][s] = weight_at(w.w1, false, (32u * M + col) * 4u + s);
+#pragma unroll
+        for (int Mo = 0; Mo < 2; ++Mo)
+#pragma unroll
+            for (int Mi = 0; Mi < 2; ++Mi)
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    a2[Mo][Mi][i] = weight_at(w.w2, false, (32u * Mo + col) * 64u + acc_row(Mi, i, h));
+#pragma unroll
+        for (int o = 0; o < 2; ++o)
+#pragma unroll
+            for (int Mi = 0; Mi < 2; ++Mi)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) w3[o][Mi][i] = weight_at(w.w3, false, (uint32_t)o * 64u + acc_row(Mi, i, h));
+        b3_0 = w.b3 ? w.b3[0] : 0.0f;
+        b3_1 = w.b3 ? w.b3[1] : 0.0f;
+    }
+
+    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, uint32_t lane) const
+    {
+        const uint32_t h = lane / 32u;
+        const float own[4] = {obs.x, obs.xd, obs.th, obs.thd};
+        float part[2][2];   // [tile][logit]: this lane's half of the layer-3 sums
+#pragma unroll
+        for (uint32_t T = 0; T < 2u; ++T) {
+            floatx16 c1[2];
+#pragma unroll
+            for (int M = 0; M < 2; ++M) {
+                c1[M] = bias_tile(lds_b1, M, h);
+                // K step s: lanes of half T supply obs[s] (k = T), the other half 0
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    c1[M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][s], h == T ? own[s] : 0.0f, c1[M], 0, 0, 0);
+            }
+#pragma unroll
+            for (int M = 0; M < 2; ++M)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) c1[M][i] = tanh_fast(c1[M][i]);
+            floatx16 c2[2];
+#pragma unroll
+            for (int Mo = 0; Mo < 2; ++Mo) {
+                c2[Mo] = bias_tile(lds_b2, Mo, h);
+#pragma unroll
+                for (int Mi = 0; Mi < 2; ++Mi)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2[Mo][Mi][i], c1[Mi][i], c2[Mo], 0, 0, 0);
+            }
+            float p_0 = 0.0f, p_1 = 0.0f;
+#pragma unroll
+            for (int Mi = 0; Mi < 2; ++Mi)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float v = tanh_fast(c2[Mi][i]);
+                    p_0 = __builtin_fmaf(w3[0][Mi][i], v, p_0);
+                    p_1 = __builtin_fmaf(w3[1][Mi][i], v, p_1);
+                }
+            part[T][0] = p_0;
+            part[T][1] = p_1;
+        }
+        // this lane's environment is column lane%32 of tile h; the other half of
+        // its hidden units was summed by lane ^ 32 as that lane's "other tile"
+        const float send0 = h ? part[0][0] : part[1][0];
+        const float send1 = h ? part[0][1] : part[1][1];
+        const float recv0 = __shfl_xor(send0, 32, 64);
+        const float recv1 = __shfl_xor(send1, 32, 64);
+        const float l0 = (h ? part[1][0] : part[0][0]) + recv0 + b3_0;
+        const float l1 = (h ? part[1][1] : part[0][1]) + recv1 + b3_1;
+        const float e = __builtin_amdgcn_exp2f((l1 - l0) * 1.44269504088896340736f);
+        return __builtin_amdgcn_rcpf(1.0f + e);
+    }
+};
+
+// Fused policy + cart-pole kernel.  Every lane takes part in the MLP (the
+// matrix instructions need the whole wave); lanes past n_envs carry a zero
+// state and store nothing.
+template <class Mlp, bool REC, bool STATS, bool P0>
+__global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs w)
+{
+    __shared__ float lds_b1[64];
+    __shared__ float lds_b2[64];
+    if (threadIdx.x < 64u) {
+        lds_b1[threadIdx.x] = w.b1 ? w.b1[threadIdx.x] : 0.0f;
+        lds_b2[threadIdx.x] = w.b2 ? w.b2[threadIdx.x] : 0.0f;
+    }
+    __syncthreads();
+
+    const uint32_t blk = xcd_block();
+    const uint32_t env = blk * kBlock + threadIdx.x;
+    const uint32_t lane = threadIdx.x % 64u;
+    const bool live = env < a.n;
+    const DevParams& p = a.p;
+
+    Mlp mlp;
+    mlp.load(w, lane);
+
+    CartCore<REC, STATS> core(p, env);
+    if (live) {
+        core.load(a);
+    } else {
+        core.s = CartState{0.0f, 0.0f, 0.0f, 0.0f};
+        core.ep = 0u;
+        core.ep_start = 0u;
+    }
+    if (REC) core.set_rows(a, 0);
+    float* p0_row = w.p0;
+    uint4 pw = make_uint4(0u, 0u, 0u, 0u);
+    NoPad nopad;
+    for (uint32_t k = 0; k < a.K; ++k) {
+        const uint32_t t = a.t0 + k;
+        if (k == 0u || ((t + 1u) & 7u) == 0u) core.draw_reset((t + 1u) >> 3);
+        if (k == 0u || (t & 3u) == 0u) pw = philox(env, t >> 2, STREAM_POLICY, p.key0, p.key1);
+        const float u = u24(pick_word(pw, t & 3u));
+        const float p0 = mlp.p0(core.s, lds_b1, lds_b2, lane);
+        const uint32_t act = (u < p0) ? 0u : 1u;
+        if (live) {
+            if (P0) *at(p0_row, env * 4u) = p0;
+            core.step_with(act, nopad);
+        }
+        // row pointers stay wave-uniform: advanced outside the lane branch
+        if (P0) p0_row += a.n;
+        if (REC) core.advance_rows();
+    }
+    if (live) core.store(a);
+    if (STATS) {
+        const uint32_t len_sum = live ? core.finished_length_sum(a.K) : 0u;
+        store_block_stats(a.stats, blk, core.n_eps, len_sum, core.n_term, core.n_trunc);
+    }
+}
+
+}  // namespace rlsim_dev

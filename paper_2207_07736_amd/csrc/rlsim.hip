@@ -12,7 +12,7 @@
 #include <string>
 #include <vector>
 
-#include "k_cartpole.hip.h"
+#include "k_policy.hip.h"
 
 using namespace rlsim_dev;
 
@@ -182,6 +182,24 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
     return hipGetLastError();
 }
 
+template <class Mlp, bool REC, bool STATS>
+hipError_t launch_policy(const StepArgs& a, const PolicyArgs& w, hipStream_t s)
+{
+    const dim3 grid(grid_for(a.n)), block(kBlock);
+    if (w.p0) hipLaunchKernelGGL((k_policy_fused<Mlp, REC, STATS, true>), grid, block, 0, s, a, w);
+    else hipLaunchKernelGGL((k_policy_fused<Mlp, REC, STATS, false>), grid, block, 0, s, a, w);
+    return hipGetLastError();
+}
+
+template <class Mlp>
+hipError_t launch_policy_any(const StepArgs& a, const PolicyArgs& w, bool rec, bool stats, hipStream_t s)
+{
+    if (rec && stats) return launch_policy<Mlp, true, true>(a, w, s);
+    if (rec) return launch_policy<Mlp, true, false>(a, w, s);
+    if (stats) return launch_policy<Mlp, false, true>(a, w, s);
+    return launch_policy<Mlp, false, false>(a, w, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -299,7 +317,18 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     if (!aligned4(tr.obs) || !aligned4(tr.reward) || !aligned4(tr.block_stats) || !aligned4(tr.policy_p0))
         return fail(h, RLSIM_EINVAL, "rlsim_step_fused: f32/u32 pointers must be 4-byte aligned");
     if (tr.policy_p0 && !policy) return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy_p0 needs a policy");
-    if (policy) return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: policy kernels not built yet");
+    if (policy) {
+        if (policy->dtype != RLSIM_F32 && policy->dtype != RLSIM_BF16)
+            return fail(h, RLSIM_EINVAL, "rlsim_step_fused: unknown policy dtype");
+        if (!policy->w1 || !policy->w2 || !policy->w3)
+            return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy weights must not be NULL");
+        const size_t wal = policy->dtype == RLSIM_F32 ? 4 : 2;
+        if (((uintptr_t)policy->w1 | (uintptr_t)policy->w2 | (uintptr_t)policy->w3) % wal != 0 ||
+            !aligned4(policy->b1) || !aligned4(policy->b2) || !aligned4(policy->b3))
+            return fail(h, RLSIM_EINVAL, "rlsim_step_fused: misaligned policy arrays");
+        if (h->D != 0u)
+            return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: a policy with padding words is not supported");
+    }
 
     DeviceGuard g(h->device);
     if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_step_fused: cannot select the handle's device");
@@ -322,6 +351,14 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     a.stats = tr.block_stats;
     const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
     hipError_t e;
+    if (policy) {
+        PolicyArgs w{policy->w1, policy->b1, policy->w2, policy->b2, policy->w3, policy->b3, tr.policy_p0};
+        e = policy->dtype == RLSIM_BF16 ? launch_policy_any<MlpBf16>(a, w, rec, stats, h->stream)
+                                        : launch_policy_any<MlpF32>(a, w, rec, stats, h->stream);
+        if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");
+        h->t += K;
+        return RLSIM_OK;
+    }
     if (rec && stats) e = launch_step<true, true>(a, h->wide, h->stream);
     else if (rec) e = launch_step<true, false>(a, h->wide, h->stream);
     else if (stats) e = launch_step<false, true>(a, h->wide, h->stream);
