@@ -204,7 +204,93 @@ def fusion_sweeps(stream) -> dict:
         print(f"[bench] sweep D={D}: K1 {entry['K1']['ms']:.2f} ms, K500 {entry['K500']['ms']:.2f} ms", file=sys.stderr,
               flush=True)
     out[w["name"]] = d_rows
+
+    out[workloads.WORKLOADS["C5"]["name"]] = policy_sweep(stream)
     return out
+
+
+MLP_FLOPS_PER_ENV_STEP = 2 * (64 * 4 + 64 * 64 + 2 * 64)
+
+
+def policy_only(dtype: str, steps: int, warmup: int) -> int:
+    """Timed runs of the MLP-policy workload alone (for profiling): each run is
+    the 256 steps of 1,048,576 envs in 16 launches of K = 16."""
+    import torch
+    from paper_2207_07736_amd import RLSIM_BF16, RLSIM_F32, Simulator, Trajectory, policy_struct
+    w = workloads.WORKLOADS["C5"]
+    n, T, K = w["n"], w["T"], w["K"][0]
+    stream = torch.cuda.current_stream()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    wts = workloads.mlp_weights(w["seed"])
+    keep = {k: (torch.from_numpy(v).cuda().to(tdt) if k.startswith("w") else torch.from_numpy(v).cuda()).contiguous()
+            for k, v in wts.items()}
+    pol = policy_struct(RLSIM_BF16 if dtype == "bf16" else RLSIM_F32, keep["w1"], keep["b1"], keep["w2"], keep["b2"],
+                        keep["w3"], keep["b3"])
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    structs = [traj.rows(k0, K) for k0 in range(0, T, K)]
+    for _ in range(warmup):
+        for st in structs:
+            sim.step(K, st, policy=pol)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        for st in structs:
+            sim.step(K, st, policy=pol)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    print(json.dumps({"workload": w["name"], "dtype": dtype, "ms_per_run": ms, "launch_ms": ms / len(structs),
+                      "env_steps_per_s": n * T / (ms * 1e-3),
+                      "mlp_TFLOPs": n * T * MLP_FLOPS_PER_ENV_STEP / (ms * 1e-3) / 1e12}), flush=True)
+    del traj
+    sim.close()
+    return 0
+
+
+def policy_sweep(stream) -> dict:
+    """The MLP-policy workload: 1,048,576 envs x 256 steps, fused K = 16 against
+    unfused K = 1, fp32 and bf16 weights ~ N(0, 1/fan_in), zero biases."""
+    from paper_2207_07736_amd import RLSIM_BF16, RLSIM_F32, Simulator, Trajectory, policy_struct
+    import torch
+    w = workloads.WORKLOADS["C5"]
+    n, T = w["n"], w["T"]
+    wts = workloads.mlp_weights(w["seed"])
+    rows = {}
+    for dtype in ("f32", "bf16"):
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        dev = {k: torch.from_numpy(v).to("cuda") for k, v in wts.items()}
+        keep = {k: (dev[k].to(tdt) if k.startswith("w") else dev[k]).contiguous() for k in dev}
+        pol = policy_struct(RLSIM_BF16 if dtype == "bf16" else RLSIM_F32, keep["w1"], keep["b1"], keep["w2"],
+                            keep["b2"], keep["w3"], keep["b3"])
+        sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+        sim.reset(w["seed"])
+        traj = Trajectory(T, n)
+        entry = {}
+        for K in (16, 1):
+            structs = [traj.rows(k0, K) for k0 in range(0, T, K)]
+            times = []
+            for r in range(3):
+                start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                start.record(stream)
+                for st in structs:
+                    sim.step(K, st, policy=pol)
+                stop.record(stream)
+                torch.cuda.synchronize()
+                if r:
+                    times.append(start.elapsed_time(stop))
+            ms = min(times)
+            entry[f"K{K}"] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3),
+                              "mlp_TFLOPs": n * T * MLP_FLOPS_PER_ENV_STEP / (ms * 1e-3) / 1e12}
+        entry["fusion_speedup"] = entry["K1"]["ms"] / entry["K16"]["ms"]
+        rows[dtype] = entry
+        del traj
+        sim.close()
+        print(f"[bench] policy {dtype}: K16 {entry['K16']['ms']:.2f} ms, K1 {entry['K1']['ms']:.2f} ms",
+              file=sys.stderr, flush=True)
+    return rows
 
 
 def main() -> int:
@@ -219,9 +305,14 @@ def main() -> int:
     ap.add_argument("--cpu-slices", type=int, default=8)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain device copy of 1 GiB (HBM counter calibration)")
+    ap.add_argument("--policy", choices=("f32", "bf16"),
+                    help="time only the MLP-policy workload (K = 16 launches) in this precision")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM traffic summary from two rocprofv3 counter CSVs and exit")
     args = ap.parse_args()
+
+    if args.policy:
+        return policy_only(args.policy, args.steps, args.warmup)
 
     if args.ingest_pmc:
         w = workloads.WORKLOADS["C3"]

@@ -28,6 +28,7 @@ FLAGS = [
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-fno-gpu-flush-denormals-to-zero",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",   # MFMA accumulators in VGPRs: no AGPR copies before tanh
     "-Wall",
     "-Wno-unused-command-line-argument",
 ]

@@ -111,7 +111,10 @@ struct MlpBf16 {
     }
 
     // p0 of this lane's environment; obs is this lane's pre-step state.
-    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, uint32_t lane) const
+    static constexpr int kW3 = 1;
+    __device__ static void fill_w3(const PolicyArgs&, float*) {}
+
+    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, const float*, uint32_t lane) const
     {
         const uint32_t h = lane / 32u;
         const bf16x8 zero8 = {};
@@ -166,12 +169,24 @@ struct MlpBf16 {
 
 // ---------------------------------------------------------------------------
 // fp32 MLP: layers 1 and 2 on v_mfma_f32_32x32x2_f32, layer 3 on the VALU.
+// Both column tiles go through each layer together, so layer 2 runs as four
+// independent accumulation chains that keep the matrix pipeline busy.
 // ---------------------------------------------------------------------------
 struct MlpF32 {
     float a1[2][4];      // layer 1 [row tile][obs index]; both halves hold the same weight
     float a2[2][2][16];  // layer 2 [out tile][in tile][accumulator register]
-    float w3[2][2][16];  // layer 3 [logit][in tile][accumulator register]
     float b3_0, b3_1;
+
+    // Output-layer weights a lane of half h needs, [logit][in tile][half][register]:
+    // W3[o][acc_row(Mi, i, h)]; filled once per workgroup.
+    static constexpr int kW3 = 2 * 2 * 2 * 16;
+    __device__ static void fill_w3(const PolicyArgs& w, float* lds_w3)
+    {
+        for (uint32_t q = threadIdx.x; q < (uint32_t)kW3; q += kBlock) {
+            const uint32_t o = q / 64u, Mi = (q / 32u) % 2u, h = (q / 16u) % 2u, i = q % 16u;
+            lds_w3[q] = weight_at(w.w3, false, o * 64u + acc_row(Mi, i, h));
+        }
+    }
 
     __device__ void load(const PolicyArgs& w, uint32_t lane)
     {
@@ -187,58 +202,62 @@ struct MlpF32 {
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
                     a2[Mo][Mi][i] = weight_at(w.w2, false, (32u * Mo + col) * 64u + acc_row(Mi, i, h));
-#pragma unroll
-        for (int o = 0; o < 2; ++o)
-#pragma unroll
-            for (int Mi = 0; Mi < 2; ++Mi)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) w3[o][Mi][i] = weight_at(w.w3, false, (uint32_t)o * 64u + acc_row(Mi, i, h));
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
     }
 
-    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, uint32_t lane) const
+    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, const float* lds_w3,
+                        uint32_t lane) const
     {
         const uint32_t h = lane / 32u;
         const float own[4] = {obs.x, obs.xd, obs.th, obs.thd};
-        float part[2][2];   // [tile][logit]: this lane's half of the layer-3 sums
+        // layer 1, both tiles: K step s takes obs[s] from the tile's own half (k = T), 0 from the other
+        floatx16 c1[2][2];
 #pragma unroll
-        for (uint32_t T = 0; T < 2u; ++T) {
-            floatx16 c1[2];
+        for (uint32_t T = 0; T < 2u; ++T)
 #pragma unroll
             for (int M = 0; M < 2; ++M) {
-                c1[M] = bias_tile(lds_b1, M, h);
-                // K step s: lanes of half T supply obs[s] (k = T), the other half 0
+                c1[T][M] = bias_tile(lds_b1, M, h);
 #pragma unroll
                 for (int s = 0; s < 4; ++s)
-                    c1[M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][s], h == T ? own[s] : 0.0f, c1[M], 0, 0, 0);
+                    c1[T][M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][s], h == T ? own[s] : 0.0f, c1[T][M], 0, 0, 0);
             }
+#pragma unroll
+        for (int T = 0; T < 2; ++T)
 #pragma unroll
             for (int M = 0; M < 2; ++M)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) c1[M][i] = tanh_fast(c1[M][i]);
-            floatx16 c2[2];
+                for (int i = 0; i < 16; ++i) c1[T][M][i] = tanh_fast(c1[T][M][i]);
+        // layer 2: four independent chains [tile][out row tile]
+        floatx16 c2[2][2];
 #pragma unroll
-            for (int Mo = 0; Mo < 2; ++Mo) {
-                c2[Mo] = bias_tile(lds_b2, Mo, h);
+        for (int T = 0; T < 2; ++T)
 #pragma unroll
-                for (int Mi = 0; Mi < 2; ++Mi)
+            for (int Mo = 0; Mo < 2; ++Mo) c2[T][Mo] = bias_tile(lds_b2, Mo, h);
 #pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2[Mo][Mi][i], c1[Mi][i], c2[Mo], 0, 0, 0);
-            }
-            float p_0 = 0.0f, p_1 = 0.0f;
+        for (int Mi = 0; Mi < 2; ++Mi)
 #pragma unroll
-            for (int Mi = 0; Mi < 2; ++Mi)
+            for (int i = 0; i < 16; ++i)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float v = tanh_fast(c2[Mi][i]);
-                    p_0 = __builtin_fmaf(w3[0][Mi][i], v, p_0);
-                    p_1 = __builtin_fmaf(w3[1][Mi][i], v, p_1);
+                for (int T = 0; T < 2; ++T)
+#pragma unroll
+                    for (int Mo = 0; Mo < 2; ++Mo)
+                        c2[T][Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2[Mo][Mi][i], c1[T][Mi][i], c2[T][Mo], 0, 0, 0);
+        // layer 3 on the VALU: this lane's half of the hidden units, for both tiles
+        float part[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};   // [tile][logit]
+#pragma unroll
+        for (int Mi = 0; Mi < 2; ++Mi)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float w0 = lds_w3[(0 * 2 + Mi) * 32 + h * 16 + i];
+                const float w1 = lds_w3[(1 * 2 + Mi) * 32 + h * 16 + i];
+#pragma unroll
+                for (int T = 0; T < 2; ++T) {
+                    const float v = tanh_fast(c2[T][Mi][i]);
+                    part[T][0] = __builtin_fmaf(w0, v, part[T][0]);
+                    part[T][1] = __builtin_fmaf(w1, v, part[T][1]);
                 }
-            part[T][0] = p_0;
-            part[T][1] = p_1;
-        }
+            }
         // this lane's environment is column lane%32 of tile h; the other half of
         // its hidden units was summed by lane ^ 32 as that lane's "other tile"
         const float send0 = h ? part[0][0] : part[1][0];
@@ -260,10 +279,12 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
 {
     __shared__ float lds_b1[64];
     __shared__ float lds_b2[64];
+    __shared__ float lds_w3[Mlp::kW3];
     if (threadIdx.x < 64u) {
         lds_b1[threadIdx.x] = w.b1 ? w.b1[threadIdx.x] : 0.0f;
         lds_b2[threadIdx.x] = w.b2 ? w.b2[threadIdx.x] : 0.0f;
     }
+    Mlp::fill_w3(w, lds_w3);
     __syncthreads();
 
     const uint32_t blk = xcd_block();
@@ -292,7 +313,7 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
         if (k == 0u || ((t + 1u) & 7u) == 0u) core.draw_reset((t + 1u) >> 3);
         if (k == 0u || (t & 3u) == 0u) pw = philox(env, t >> 2, STREAM_POLICY, p.key0, p.key1);
         const float u = u24(pick_word(pw, t & 3u));
-        const float p0 = mlp.p0(core.s, lds_b1, lds_b2, lane);
+        const float p0 = mlp.p0(core.s, lds_b1, lds_b2, lds_w3, lane);
         const uint32_t act = (u < p0) ? 0u : 1u;
         if (live) {
             if (P0) *at(p0_row, env * 4u) = p0;
