@@ -33,12 +33,16 @@ def traffic_file(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"hbm_traffic__{workload}.txt")
 
 
+# sources of the fused random-action kernel the headline times
+FUSED_KERNEL_SOURCES = ("device_common.hip.h", "k_cartpole.hip.h")
+
+
 def kernel_source_digest() -> str:
-    """Digest of the kernel sources: a stored traffic measurement is used only
-    while the kernels it was taken on are unchanged."""
+    """Digest of the fused kernel's sources: a stored traffic measurement is used
+    only while the kernel it was taken on is unchanged."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2207_07736_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in FUSED_KERNEL_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
@@ -161,6 +165,30 @@ def _time_schedule(sim, traj, sched, stream, reps):
     return times[len(times) // 2]
 
 
+def _graph_ms(sim, structs, stream, reps: int) -> float:
+    """Median time of replaying one HIP graph that holds the K = 1 launches of
+    `structs` (one kernel node per rlsim_step_fused call)."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        for st in structs:
+            sim.step(1, st)
+    g.replay()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        g.replay()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        times.append(start.elapsed_time(stop))
+    del g
+    times.sort()
+    return times[len(times) // 2]
+
+
 def fusion_sweeps(stream) -> dict:
     """Fused versus unfused on the K sweep (65,536 envs x 1,000 steps) and the
     state-size sweep (262,144 envs x 500 steps, D padding words per env)."""
@@ -178,6 +206,8 @@ def fusion_sweeps(stream) -> dict:
     base = rows["1"]["ms"]
     for r in rows.values():
         r["speedup_vs_K1"] = base / r["ms"]
+    gms = _graph_ms(sim, [traj.rows(k, 1) for k in range(T)], stream, 3)
+    rows["1_hipgraph"] = {"ms": gms, "env_steps_per_s": n * T / (gms * 1e-3), "speedup_vs_K1": base / gms}
     out[w["name"]] = rows
     del traj
     sim.close()
@@ -206,7 +236,32 @@ def fusion_sweeps(stream) -> dict:
     out[w["name"]] = d_rows
 
     out[workloads.WORKLOADS["C5"]["name"]] = policy_sweep(stream)
+    out[workloads.C_SWEEP["name"]] = compute_factor_sweep(stream)
     return out
+
+
+def compute_factor_sweep(stream) -> dict:
+    """Fused (K = 100) against unfused (K = 1) as the compute factor C grows:
+    65,536 envs x 100 steps, each step C Euler iterations of tau / C."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.C_SWEEP
+    n, T = w["n"], w["T"]
+    rows = {}
+    for C in w["C"]:
+        sim = Simulator(n, 0, workloads.cartpole(compute_factor=C), stream=stream)
+        sim.reset(w["seed"])
+        traj = Trajectory(T, n)
+        entry = {}
+        for K in w["K"]:
+            ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=2)
+            entry[f"K{K}"] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3)}
+        entry["fusion_speedup"] = entry["K1"]["ms"] / entry[f"K{T}"]["ms"]
+        rows[f"C{C}"] = entry
+        del traj
+        sim.close()
+    print("[bench] compute-factor sweep: " + ", ".join(f"{k} {v['fusion_speedup']:.2f}x" for k, v in rows.items()),
+          file=sys.stderr, flush=True)
+    return rows
 
 
 MLP_FLOPS_PER_ENV_STEP = 2 * (64 * 4 + 64 * 64 + 2 * 64)
@@ -335,7 +390,10 @@ def main() -> int:
     w = workloads.WORKLOADS["C3"]
     n, T, K = w["n"], w["T"], w["K"][0]
     seed = w["seed"]
-    stream = torch.cuda.current_stream()
+    # one side stream for every launch and every timing event (graph capture
+    # needs a stream other than the legacy default one)
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
 
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
     sim.reset(seed)
@@ -403,8 +461,10 @@ def main() -> int:
         stop.record(stream)
         torch.cuda.synchronize()
         unfused_ms = start.elapsed_time(stop) / reps
-        result["fusion"] = {"unfused_K1_ms": unfused_ms, "fused_K200_ms": ms_per_step,
+        graph_ms = _graph_ms(sim, row_structs, stream, reps)
+        result["fusion"] = {"unfused_K1_ms": unfused_ms, "unfused_K1_hipgraph_ms": graph_ms, "fused_K200_ms": ms_per_step,
                             "speedup": unfused_ms / ms_per_step,
+                            "speedup_over_hipgraph": graph_ms / ms_per_step,
                             "unfused_algorithmic_GBs": (n * T * (workloads.TRAJ_BYTES_PER_ENV_STEP + 40)) / (unfused_ms * 1e-3) / 1e9}
 
     del traj

@@ -50,7 +50,8 @@ typedef struct rlsim rlsim_t;                 /* opaque handle */
  * stream the handle enqueues on.  rlsim_cfg_default fills the classic values:
  * g = 9.8, cart 1.0, pole 0.1, half length 0.5, force 10, tau 0.02, |x| limit
  * 2.4, |theta| limit = fp32(12 * 2 pi / 360), 500-step episodes, reset box
- * [-0.05, 0.05), padding a in [0.9, 0.99), b in [-1, 1), flags 0, stream NULL. */
+ * [-0.05, 0.05), padding a in [0.9, 0.99), b in [-1, 1), flags 0, compute
+ * factor 1, stream NULL. */
 typedef struct {
     float gravity, masscart, masspole, half_length, force_mag, tau;
     float x_threshold, theta_threshold_rad;
@@ -59,6 +60,9 @@ typedef struct {
     float pad_a_low, pad_a_high;           /* padding decay a_j */
     float pad_b_low, pad_b_high;           /* padding gain b_j */
     uint32_t flags;                        /* RLSIM_F_* */
+    uint32_t compute_factor;               /* C >= 1: each step is C Euler iterations of
+                                              length tau / C (the paper's compute factor,
+                                              "Simulator Complexity"); default 1 */
     void* stream;                          /* hipStream_t; NULL = default stream */
 } rlsim_cfg;
 
@@ -71,7 +75,8 @@ void rlsim_cfg_default(rlsim_cfg* cfg);
  * environment) on the device.  cfg may be NULL (defaults).
  * Errors: EINVAL if out == NULL, n_envs == 0 or n_envs > 2^30, state_words < 4,
  * a non-finite or inconsistent constant (masses <= 0, half_length <= 0,
- * reset_low > reset_high, ...); ENOMEM; EDEVICE.  On error *out is NULL. */
+ * reset_low > reset_high, compute_factor == 0, ...); ENOMEM; EDEVICE.  On error
+ * *out is NULL. */
 int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rlsim_t** out);
 
 /* Start every environment's first episode at global step t = 0 (Background,

@@ -12,7 +12,8 @@ Training"; K steps per call as in "Simulator Kernel Fusion"):
 
 * ``philox4x32_10`` -- the counter-based generator of Salmon et al. (SC'11).
 * ``cartpole_step`` -- one explicit-Euler step of the frictionless cart and
-  uniform rod, fp32, each operation rounded once.
+  uniform rod, fp32, each operation rounded once; ``env_step`` -- a simulation
+  step made of C such iterations of length tau / C (the compute factor).
 * ``Sim`` -- N environments with auto-reset, the random-action or MLP-policy
   loop, padding words (the paper's state-size factor S, Simulator Complexity)
   and per-256-env block statistics.
@@ -54,6 +55,7 @@ class Params(ctypes.Structure):
         ("pad_a_low", ctypes.c_float), ("pad_a_high", ctypes.c_float),
         ("pad_b_low", ctypes.c_float), ("pad_b_high", ctypes.c_float),
         ("no_termination", ctypes.c_uint32),
+        ("compute_factor", ctypes.c_uint32),
     ]
 
 
@@ -88,6 +90,8 @@ def lib():
     L.orc_cos.restype = ctypes.c_float
     L.orc_cartpole_step.argtypes = [ctypes.POINTER(Params), f32p, ctypes.c_int, f32p]
     L.orc_cartpole_step.restype = None
+    L.orc_env_step.argtypes = [ctypes.POINTER(Params), f32p, ctypes.c_int, f32p]
+    L.orc_env_step.restype = None
     L.orc_terminated.argtypes = [ctypes.POINTER(Params), f32p]
     L.orc_terminated.restype = ctypes.c_int
     L.orc_reset_draw.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, f32p]
@@ -174,6 +178,15 @@ def cartpole_step(params: Params, state, action: int) -> np.ndarray:
     out = np.zeros(4, dtype=np.float32)
     P = ctypes.POINTER(ctypes.c_float)
     lib().orc_cartpole_step(ctypes.byref(params), s.ctypes.data_as(P), int(action), out.ctypes.data_as(P))
+    return out
+
+
+def env_step(params: Params, state, action: int) -> np.ndarray:
+    """One simulation step: compute_factor Euler iterations of tau / C."""
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    out = np.zeros(4, dtype=np.float32)
+    P = ctypes.POINTER(ctypes.c_float)
+    lib().orc_env_step(ctypes.byref(params), s.ctypes.data_as(P), int(action), out.ctypes.data_as(P))
     return out
 
 

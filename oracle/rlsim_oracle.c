@@ -88,6 +88,7 @@ typedef struct {
     float reset_low, reset_high;
     float pad_a_low, pad_a_high, pad_b_low, pad_b_high;
     uint32_t no_termination;         /* nonzero: termination never fires */
+    uint32_t compute_factor;         /* C >= 1 Euler sub-iterations of tau / C per step */
 } orc_params;
 
 /* ------------------------------------------------------------------------ */
@@ -166,6 +167,23 @@ void orc_cartpole_step(const orc_params* p, const float in[4], int action, float
     out[1] = fmaf(p->tau, xacc, xd);
     out[2] = fmaf(p->tau, thd, th);
     out[3] = fmaf(p->tau, thacc, thd);
+}
+
+/* One simulation step with the paper's compute factor C ("Simulator       */
+/* Complexity"): C explicit-Euler iterations of length tau / C (one fp32    */
+/* division), the action held for all of them.  C = 1 is the plain step.   */
+void orc_env_step(const orc_params* p, const float in[4], int action, float out[4])
+{
+    uint32_t C = p->compute_factor;
+    orc_params sub = *p;
+    sub.tau = p->tau / (float)C;
+    float cur[4] = { in[0], in[1], in[2], in[3] };
+    for (uint32_t c = 0; c < C; ++c) {
+        float nxt[4];
+        orc_cartpole_step(&sub, cur, action, nxt);
+        for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
+    }
+    for (int q = 0; q < 4; ++q) out[q] = cur[q];
 }
 
 /* Strict threshold test on the post-step state; NaN compares false. */
@@ -314,7 +332,7 @@ void orc_destroy(orc_sim* sim)
 
 orc_sim* orc_create(uint32_t n, uint32_t env0, uint32_t D, const orc_params* p)
 {
-    if (n == 0) return NULL;
+    if (n == 0 || p->compute_factor == 0) return NULL;
     orc_sim* sim = (orc_sim*)calloc(1, sizeof(orc_sim));
     if (!sim) return NULL;
     sim->n = n; sim->env0 = env0; sim->D = D; sim->p = *p;
@@ -397,7 +415,7 @@ int orc_step(orc_sim* sim, uint32_t K, const orc_policy* pol,
                 a = orc_action_bit(sim->seed, env, t);
             }
 
-            orc_cartpole_step(&sim->p, cur, a, nxt);
+            orc_env_step(&sim->p, cur, a, nxt);
             for (uint32_t j = 0; j < sim->D; ++j) {
                 size_t q = (size_t)j * n + i;
                 sim->s[q] = orc_pad_update(sim->s[q], sim->a[q], sim->b[q], a);

@@ -12,7 +12,8 @@ namespace rlsim_dev {
 // fp32 operation (see make_dev_params in rlsim.hip).
 // ---------------------------------------------------------------------------
 struct DevParams {
-    float gravity, force_mag, tau, half_length;
+    float gravity, force_mag, tau, half_length;   // tau here is the iteration length tau / C
+    uint32_t iters;       // compute factor C: Euler iterations per simulation step
     float pole_ml;        // masspole * half_length
     float inv_total;      // 1 / (masscart + masspole)
     float m_over_M;       // masspole * inv_total

@@ -119,7 +119,9 @@ struct CartCore {
     template <class Hook>
     __device__ __forceinline__ void step_with(uint32_t act, Hook& hook)
     {
-        const CartState nx = cartpole_step(p, s, act);
+        CartState nx = cartpole_step(p, s, act);
+        // compute factor C > 1: the remaining Euler iterations of the step
+        for (uint32_t c = 1; c < p.iters; ++c) nx = cartpole_step(p, nx, act);
         const uint32_t len = ep + 1u;
         const bool term = crossed(p, nx);
         const bool trunc = (p.max_steps != 0u) && (len >= p.max_steps);

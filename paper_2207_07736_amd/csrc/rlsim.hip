@@ -80,9 +80,11 @@ DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
     volatile float m_over_M = c.masspole * inv_total;
     volatile float ml_over_M = pole_ml * inv_total;
     volatile float width = c.reset_high - c.reset_low;
+    volatile float tau_iter = c.tau / (float)c.compute_factor;
     p.gravity = c.gravity;
     p.force_mag = c.force_mag;
-    p.tau = c.tau;
+    p.tau = tau_iter;
+    p.iters = c.compute_factor;
     p.half_length = c.half_length;
     p.pole_ml = pole_ml;
     p.inv_total = inv_total;
@@ -119,6 +121,7 @@ const char* check_cfg(const rlsim_cfg& c)
     }
     if (c.pad_a_low > c.pad_a_high || c.pad_b_low > c.pad_b_high) return "cfg: padding range low > high";
     if ((c.flags & ~(uint32_t)RLSIM_F_NO_TERMINATION) != 0u) return "cfg: unknown flag bits";
+    if (c.compute_factor == 0u) return "cfg: compute_factor must be >= 1";
     return nullptr;
 }
 
@@ -223,6 +226,7 @@ void rlsim_cfg_default(rlsim_cfg* c)
     c->pad_b_low = -1.0f;
     c->pad_b_high = 1.0f;
     c->flags = 0u;
+    c->compute_factor = 1u;
     c->stream = nullptr;
 }
 

@@ -45,6 +45,7 @@ class rlsim_cfg(ctypes.Structure):
         ("pad_a_low", ctypes.c_float), ("pad_a_high", ctypes.c_float),
         ("pad_b_low", ctypes.c_float), ("pad_b_high", ctypes.c_float),
         ("flags", ctypes.c_uint32),
+        ("compute_factor", ctypes.c_uint32),
         ("stream", ctypes.c_void_p),
     ]
 

@@ -150,3 +150,13 @@ def test_state_and_argument_errors_with_handle():
         del tr
     finally:
         sim.close()
+
+
+def test_create_rejects_zero_compute_factor():
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    assert c.compute_factor == 1
+    c.compute_factor = 0
+    with pytest.raises(p.RlsimError) as e:
+        p.rlsim_create(8, 4, c)
+    assert e.value.code == p.RLSIM_EINVAL

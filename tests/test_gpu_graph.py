@@ -1,0 +1,62 @@
+"""K unfused launches captured in a HIP graph (the decomposition of the fusion
+speedup into launch overhead and register residency).
+
+rlsim_step_fused issues exactly one kernel launch and no memset or allocation,
+so a sequence of calls on a capturing stream records one kernel node per call.
+Every replay is checked against the eager run, with eager work (a reset) and a
+synchronisation between replays.
+"""
+import numpy as np
+import pytest
+
+import workloads
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2207_07736_amd  # noqa: F401
+
+
+@pytest.mark.parametrize("D", [0, 5, 40])
+def test_graph_of_unfused_launches_matches_eager(D):
+    from paper_2207_07736_amd import Simulator, Trajectory
+    n, T, seed = 3000, 60, 4
+    s = torch.cuda.Stream()
+    sim = Simulator(n, D, workloads.CARTPOLE, stream=s)
+    try:
+        tr = Trajectory(T, n)
+        rows = [tr.rows(k, 1) for k in range(T)]
+        with torch.cuda.stream(s):
+            # eager reference
+            sim.reset(seed)
+            for k in range(T):
+                sim.step(1, rows[k])
+            s.synchronize()
+            ref = {k: getattr(tr, k).clone() for k in ("obs", "action", "reward", "done")}
+            ref_state = sim.get_state()
+            # capture the same T launches (t = 0 .. T-1 are baked into the nodes)
+            sim.reset(seed)
+            s.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                for k in range(T):
+                    sim.step(1, rows[k])
+            for rep in range(3):
+                for k in ("obs", "action", "reward", "done"):
+                    getattr(tr, k).zero_()
+                sim.reset(seed)                 # eager work between replays
+                s.synchronize()
+                g.replay()
+                s.synchronize()
+                for k in ("obs", "action", "reward", "done"):
+                    assert torch.equal(getattr(tr, k), ref[k]), (rep, k)
+                st, ep, _ = sim.get_state()
+                assert np.array_equal(st.view(np.uint32), ref_state[0].view(np.uint32)) and np.array_equal(ep, ref_state[1])
+        del g, tr
+    finally:
+        sim.close()

@@ -239,3 +239,15 @@ def test_nan_state_propagates_like_oracle():
         assert np.array_equal(g_obs[fin].view(np.uint32), ref["obs"][fin].view(np.uint32))
     finally:
         sim.close()
+
+
+@pytest.mark.parametrize("C", [2, 7, 64])
+def test_compute_factor_bit_exact(C):
+    """The paper's compute factor: C Euler iterations of tau / C per step."""
+    cfg = workloads.cartpole(compute_factor=C)
+    n, T = 300, 90
+    g = gpu_run(n, T, [1, 40, 49], D=3, seed=6, cfg=cfg)
+    r = oracle_run(n, T, [1, 40, 49], D=3, seed=6, cfg=cfg)
+    assert_bit_equal(g, r)
+    for a, b in zip(g["stats"], r["stats"]):
+        assert np.array_equal(a, b)

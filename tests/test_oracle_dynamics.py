@@ -226,3 +226,53 @@ def test_thresholds_strict_and_nan():
     assert on(float("inf"), 0.0)
     noterm = oracle.make_params(**workloads.cartpole(no_termination=1))
     assert not oracle.terminated(noterm, np.array([100, 0, 3, 0], dtype=np.float32))
+
+
+def test_compute_factor_one_is_the_plain_step():
+    rng = np.random.Generator(np.random.PCG64(21))
+    for _ in range(200):
+        st = rng.uniform(-0.2, 0.2, 4).astype(np.float32)
+        a = int(rng.integers(0, 2))
+        assert np.array_equal(oracle.env_step(P, st, a), oracle.cartpole_step(P, st, a))
+
+
+def test_compute_factor_converges_first_order():
+    """C Euler iterations of tau / C approach the exact flow of the ODE over one
+    step as C grows, with error halving when C doubles (first-order method).
+    Reference: the same Euler-Lagrange mass-matrix ODE integrated with a
+    50-digit classical Runge-Kutta method on a fine grid."""
+    state0 = np.array([0.1, 0.5, 0.12, -1.5], dtype=np.float32)
+
+    def rk4_flow(y0, F, tau, steps=400):
+        c = workloads.CARTPOLE
+        with mpmath.workdps(40):
+            g, mc, m, l = (mpmath.mpf(float(F32(c[k]))) for k in ("gravity", "masscart", "masspole", "half_length"))
+            M = mc + m
+
+            def f(y):
+                x, xd, th, thd = y
+                A = mpmath.matrix([[M, m * l * mpmath.cos(th)], [m * l * mpmath.cos(th), mpmath.mpf(4) / 3 * m * l * l]])
+                rhs = mpmath.matrix([F + m * l * thd**2 * mpmath.sin(th), m * g * l * mpmath.sin(th)])
+                xa, ta = mpmath.lu_solve(A, rhs)
+                return [xd, xa, thd, ta]
+            y = [mpmath.mpf(float(v)) for v in y0]
+            h = mpmath.mpf(float(F32(tau))) / steps
+            for _ in range(steps):
+                k1 = f(y)
+                k2 = f([a + h / 2 * b for a, b in zip(y, k1)])
+                k3 = f([a + h / 2 * b for a, b in zip(y, k2)])
+                k4 = f([a + h * b for a, b in zip(y, k3)])
+                y = [a + h / 6 * (b1 + 2 * b2 + 2 * b3 + b4) for a, b1, b2, b3, b4 in zip(y, k1, k2, k3, k4)]
+            return np.array([float(v) for v in y])
+
+    # a long step (tau = 0.2) so that the discretisation error dominates rounding
+    c = workloads.cartpole(tau=0.2, no_termination=1, max_episode_steps=0)
+    exact = rk4_flow(state0, float(F32(c["force_mag"])), c["tau"])
+    errs = []
+    for C in (4, 8, 16, 32):
+        params = oracle.make_params(**dict(c, compute_factor=C))
+        got = oracle.env_step(params, state0, 1).astype(np.float64)
+        errs.append(np.abs(got - exact).max())
+    errs = np.array(errs)
+    ratios = errs[:-1] / errs[1:]
+    assert np.all((ratios > 1.7) & (ratios < 2.3)), (errs, ratios)

@@ -37,6 +37,7 @@ CARTPOLE = dict(
     pad_b_low=-1.0,
     pad_b_high=1.0,
     no_termination=0,
+    compute_factor=1,
 )
 
 
@@ -59,6 +60,10 @@ WORKLOADS = {
     "C4": dict(name="cartpole-256k-500-Dsweep", n=262144, T=500, K=[1, 500], D=[4, 64, 512, 4096], seed=0, policy=None),
     "C5": dict(name="cartpole-1M-256-K16-mlp", n=1048576, T=256, K=[16], D=[0], seed=0, policy=("f32", "bf16")),
 }
+
+# Compute-factor sweep (the paper's "Simulator Complexity", factor C): C Euler
+# iterations per step at a fixed state size, fused against unfused.
+C_SWEEP = dict(name="cartpole-64k-100-Csweep", n=65536, T=100, K=[1, 100], C=[1, 4, 16, 64, 256, 1024], seed=0)
 
 # Parity seeds: 0, 1, and one whose high 32 bits are nonzero.
 PARITY_SEEDS = (0, 1, (1 << 40) + 7)
