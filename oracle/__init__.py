@@ -61,7 +61,7 @@ class Params(ctypes.Structure):
 
 class _Policy(ctypes.Structure):
     _fields_ = [("bf16", ctypes.c_int)] + [
-        (name, ctypes.POINTER(ctypes.c_float)) for name in ("w1", "b1", "w2", "b2", "w3", "b3")
+        (name, ctypes.POINTER(ctypes.c_float)) for name in ("w1", "b1", "w2", "b2", "w3", "b3", "wv", "bv")
     ]
 
 
@@ -108,6 +108,11 @@ def lib():
     L.orc_round_bf16.restype = ctypes.c_double
     L.orc_mlp_p0.argtypes = [ctypes.POINTER(_Policy), f32p]
     L.orc_mlp_p0.restype = ctypes.c_double
+    f64p = ctypes.POINTER(ctypes.c_double)
+    L.orc_mlp_eval.argtypes = [ctypes.POINTER(_Policy), f32p, f64p, f64p, f64p]
+    L.orc_mlp_eval.restype = None
+    L.orc_log_prob.argtypes = [f64p, ctypes.c_int]
+    L.orc_log_prob.restype = ctypes.c_double
     L.orc_create.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(Params)]
     L.orc_create.restype = ctypes.c_void_p
     L.orc_destroy.argtypes = [ctypes.c_void_p]
@@ -116,7 +121,7 @@ def lib():
     L.orc_reset.restype = None
     L.orc_step.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(_Policy),
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                           ctypes.c_void_p, ctypes.c_void_p]
+                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     L.orc_step.restype = ctypes.c_int
     L.orc_get_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint64)]
     L.orc_get_state.restype = None
@@ -225,18 +230,20 @@ def round_bf16(v: float) -> float:
 
 
 class Policy:
-    """MLP weights (fp32 numpy, row-major [out][in]) for the oracle."""
+    """MLP weights (fp32 numpy, row-major [out][in]) for the oracle; wv (1 x 64)
+    and bv (1,) are the optional value head."""
 
-    def __init__(self, w1, b1, w2, b2, w3, b3, bf16: bool = False):
+    def __init__(self, w1, b1, w2, b2, w3, b3, wv=None, bv=None, bf16: bool = False):
         self._arrs = [None if x is None else np.ascontiguousarray(x, dtype=np.float32)
-                      for x in (w1, b1, w2, b2, w3, b3)]
-        shapes = [(64, 4), (64,), (64, 64), (64,), (2, 64), (2,)]
+                      for x in (w1, b1, w2, b2, w3, b3, wv, bv)]
+        shapes = [(64, 4), (64,), (64, 64), (64,), (2, 64), (2,), (1, 64), (1,)]
         for a, shp in zip(self._arrs, shapes):
             if a is not None and a.shape != shp:
                 raise ValueError(f"policy array shape {a.shape} != {shp}")
         for i in (0, 2, 4):
             if self._arrs[i] is None:
                 raise ValueError("weights may not be None")
+        self.has_value = self._arrs[6] is not None
         P = ctypes.POINTER(ctypes.c_float)
         self.struct = _Policy(int(bool(bf16)), *[
             ctypes.cast(None, P) if a is None else a.ctypes.data_as(P) for a in self._arrs])
@@ -244,6 +251,26 @@ class Policy:
     def p0(self, obs) -> float:
         o = np.ascontiguousarray(obs, dtype=np.float32)
         return float(lib().orc_mlp_p0(ctypes.byref(self.struct), o.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+
+    def eval(self, obs):
+        """(logits [2] f64, p0, value) for one observation."""
+        o = np.ascontiguousarray(obs, dtype=np.float32)
+        logit = np.zeros(2, dtype=np.float64)
+        p0 = ctypes.c_double()
+        v = ctypes.c_double()
+        lib().orc_mlp_eval(ctypes.byref(self.struct), o.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                           logit.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), ctypes.byref(p0), ctypes.byref(v))
+        return logit, float(p0.value), float(v.value)
+
+    def log_prob(self, obs, action: int) -> float:
+        logit, _, _ = self.eval(obs)
+        return log_prob(logit, action)
+
+
+def log_prob(logit, action: int) -> float:
+    """log softmax(logit)[action] for two logits."""
+    lg = np.ascontiguousarray(logit, dtype=np.float64)
+    return float(lib().orc_log_prob(lg.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(action)))
 
 
 class Sim:
@@ -281,11 +308,15 @@ class Sim:
             out["done"] = np.empty((K, n), dtype=np.uint8)
             if policy is not None:
                 out["p0"] = np.empty((K, n), dtype=np.float64)
+                out["logp"] = np.empty((K, n), dtype=np.float64)
+                if policy.has_value:
+                    out["value"] = np.empty((K, n), dtype=np.float64)
         if stats:
             out["stats"] = np.empty((self.n_blocks, 4), dtype=np.uint32)
         rc = lib().orc_step(self._h, int(K), ctypes.byref(policy.struct) if policy is not None else None,
                             ptr(out.get("obs")), ptr(out.get("action")), ptr(out.get("reward")),
-                            ptr(out.get("done")), ptr(out.get("stats")), ptr(out.get("p0")))
+                            ptr(out.get("done")), ptr(out.get("stats")), ptr(out.get("p0")),
+                            ptr(out.get("logp")), ptr(out.get("value")))
         if rc != 0:
             raise RuntimeError(f"orc_step failed ({rc})")
         return out

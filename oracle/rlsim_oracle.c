@@ -243,7 +243,9 @@ float orc_pad_update(float s, float a, float b, int u)
 
 /* ------------------------------------------------------------------------ */
 /* MLP policy 4 -> 64 -> 64 -> 2, tanh hidden layers, weights row-major     */
-/* [out][in], evaluated in double.  p0 = softmax(logits)[0].                */
+/* [out][in], evaluated in double.  p0 = softmax(logits)[0].  An optional    */
+/* value head 64 -> 1 reads the same second hidden layer (a shared trunk,    */
+/* the usual actor-critic form of the learner the collected data feeds).     */
 /* bf16 mode rounds the weights, the input and both hidden activations to    */
 /* bfloat16 (round to nearest even) at the points where a bf16 kernel holds  */
 /* them; biases and sums stay in double.                                     */
@@ -251,6 +253,7 @@ float orc_pad_update(float s, float a, float b, int u)
 typedef struct {
     int bf16;
     const float *w1, *b1, *w2, *b2, *w3, *b3;   /* biases may be NULL (zero) */
+    const float *wv, *bv;                       /* value head 1 x 64, 1; wv NULL = none */
 } orc_policy;
 
 /* Round a double to the nearest bfloat16 value (ties to even), returned as */
@@ -280,9 +283,10 @@ static double orc_w(const orc_policy* pol, const float* w, int idx)
     return pol->bf16 ? orc_round_bf16(v) : v;
 }
 
-double orc_mlp_p0(const orc_policy* pol, const float obs[4])
+/* The trunk: h2 = tanh(W2 tanh(W1 obs + b1) + b2). */
+static void orc_mlp_trunk(const orc_policy* pol, const float obs[4], double h2[64])
 {
-    double in[4], h1[64], h2[64], logit[2];
+    double in[4], h1[64];
     for (int i = 0; i < 4; ++i) in[i] = pol->bf16 ? orc_round_bf16((double)obs[i]) : (double)obs[i];
     for (int o = 0; o < 64; ++o) {
         double acc = pol->b1 ? (double)pol->b1[o] : 0.0;
@@ -296,13 +300,43 @@ double orc_mlp_p0(const orc_policy* pol, const float obs[4])
         h2[o] = tanh(acc);
         if (pol->bf16) h2[o] = orc_round_bf16(h2[o]);
     }
+}
+
+/* All policy outputs for one observation: the two logits W3 h2 + b3, p0, and  */
+/* the value Wv h2 + bv (0 if the policy has no value head).                  */
+void orc_mlp_eval(const orc_policy* pol, const float obs[4], double logit[2], double* p0, double* value)
+{
+    double h2[64];
+    orc_mlp_trunk(pol, obs, h2);
     for (int o = 0; o < 2; ++o) {
         double acc = pol->b3 ? (double)pol->b3[o] : 0.0;
         for (int i = 0; i < 64; ++i) acc += orc_w(pol, pol->w3, o * 64 + i) * h2[i];
         logit[o] = acc;
     }
     /* softmax over two logits: p0 = e^l0 / (e^l0 + e^l1) = 1 / (1 + e^(l1 - l0)) */
-    return 1.0 / (1.0 + exp(logit[1] - logit[0]));
+    *p0 = 1.0 / (1.0 + exp(logit[1] - logit[0]));
+    double v = 0.0;
+    if (pol->wv) {
+        v = pol->bv ? (double)pol->bv[0] : 0.0;
+        for (int i = 0; i < 64; ++i) v += orc_w(pol, pol->wv, i) * h2[i];
+    }
+    *value = v;
+}
+
+double orc_mlp_p0(const orc_policy* pol, const float obs[4])
+{
+    double logit[2], p0, v;
+    orc_mlp_eval(pol, obs, logit, &p0, &v);
+    return p0;
+}
+
+/* log softmax(logits)[a] = l_a - log(e^l0 + e^l1), with the larger logit    */
+/* taken out of the sum so that neither exponential overflows.               */
+double orc_log_prob(const double logit[2], int a)
+{
+    double m = logit[0] > logit[1] ? logit[0] : logit[1];
+    double lse = m + log(exp(logit[0] - m) + exp(logit[1] - m));
+    return logit[a ? 1 : 0] - lse;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -382,13 +416,15 @@ void orc_reset(orc_sim* sim, uint64_t seed)
  *            t+1, ep = 0, padding words = +0;  else ep = n.
  * Outputs (each may be NULL), rows 0..K-1 of this call:
  *   obs [K][4][n] f32, act [K][n] u8, rew [K][n] f32, done [K][n] u8,
- *   p0 [K][n] f64 (policy runs), stats [nblk][4] u32 over 256-env blocks of
+ *   p0, logp (log-probability of a_t), value [K][n] f64 (policy runs),
+ *   stats [nblk][4] u32 over 256-env blocks of
  *   global env ids: {episodes finished, sum of their lengths, terminated,
  *   truncated}; nblk = (env0+n-1)/256 - env0/256 + 1.
  * Returns 0, or -1 before reset, -2 when t + K would pass 2^32 - 1.
  */
 int orc_step(orc_sim* sim, uint32_t K, const orc_policy* pol,
-             float* obs, uint8_t* act, float* rew, uint8_t* done, uint32_t* stats, double* p0_out)
+             float* obs, uint8_t* act, float* rew, uint8_t* done, uint32_t* stats, double* p0_out,
+             double* logp_out, double* value_out)
 {
     if (!sim->has_reset) return -1;
     if ((uint64_t)sim->t + (uint64_t)K > 0xFFFFFFFFull) return -2;
@@ -407,10 +443,13 @@ int orc_step(orc_sim* sim, uint32_t K, const orc_policy* pol,
 
             int a;
             if (pol) {
-                double p0 = orc_mlp_p0(pol, cur);
+                double logit[2], p0, value;
+                orc_mlp_eval(pol, cur, logit, &p0, &value);
                 float u = orc_policy_u(sim->seed, env, t);
                 a = ((double)u < p0) ? 0 : 1;
                 if (p0_out) p0_out[(size_t)k * n + i] = p0;
+                if (logp_out) logp_out[(size_t)k * n + i] = orc_log_prob(logit, a);
+                if (value_out) value_out[(size_t)k * n + i] = value;
             } else {
                 a = orc_action_bit(sim->seed, env, t);
             }

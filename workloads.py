@@ -73,10 +73,11 @@ TRAJ_BYTES_PER_ENV_STEP = 4 * 4 + 1 + 4 + 1
 
 
 def mlp_weights(seed: int, hidden: int = 64):
-    """4 -> hidden -> hidden -> 2 weights ~ N(0, 1/fan_in), row-major [out][in],
-    zero biases, fp32.  Drawn with numpy's PCG64 generator from ``seed``."""
+    """4 -> hidden -> hidden -> 2 policy weights and the hidden -> 1 value head,
+    ~ N(0, 1/fan_in), row-major [out][in], zero biases, fp32.  Drawn with numpy's
+    PCG64 generator from ``seed`` (the value head last)."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    shapes = [(hidden, 4), (hidden, hidden), (2, hidden)]
+    shapes = [(hidden, 4), (hidden, hidden), (2, hidden), (1, hidden)]
     ws = [(rng.standard_normal(s) / math.sqrt(s[1])).astype(np.float32) for s in shapes]
     bs = [np.zeros(s[0], dtype=np.float32) for s in shapes]
-    return dict(w1=ws[0], b1=bs[0], w2=ws[1], b2=bs[1], w3=ws[2], b3=bs[2])
+    return dict(w1=ws[0], b1=bs[0], w2=ws[1], b2=bs[1], w3=ws[2], b3=bs[2], wv=ws[3], bv=bs[3])
