@@ -307,7 +307,9 @@ def policy_only(dtype: str, steps: int, warmup: int) -> int:
 
 def policy_sweep(stream) -> dict:
     """The MLP-policy workload: 1,048,576 envs x 256 steps, fused K = 16 against
-    unfused K = 1, fp32 and bf16 weights ~ N(0, 1/fan_in), zero biases."""
+    unfused K = 1, fp32 and bf16 weights ~ N(0, 1/fan_in), zero biases; and K =
+    16 again with the value head and the learner planes (log pi, value)
+    recorded."""
     from paper_2207_07736_amd import RLSIM_BF16, RLSIM_F32, Simulator, Trajectory, policy_struct
     import torch
     w = workloads.WORKLOADS["C5"]
@@ -318,14 +320,20 @@ def policy_sweep(stream) -> dict:
         tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
         dev = {k: torch.from_numpy(v).to("cuda") for k, v in wts.items()}
         keep = {k: (dev[k].to(tdt) if k.startswith("w") else dev[k]).contiguous() for k in dev}
-        pol = policy_struct(RLSIM_BF16 if dtype == "bf16" else RLSIM_F32, keep["w1"], keep["b1"], keep["w2"],
-                            keep["b2"], keep["w3"], keep["b3"])
+        code = RLSIM_BF16 if dtype == "bf16" else RLSIM_F32
+        pol_plain = policy_struct(code, keep["w1"], keep["b1"], keep["w2"], keep["b2"], keep["w3"], keep["b3"])
+        pol_value = policy_struct(code, keep["w1"], keep["b1"], keep["w2"], keep["b2"], keep["w3"], keep["b3"],
+                                  keep["wv"], keep["bv"])
         sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
         sim.reset(w["seed"])
-        traj = Trajectory(T, n)
+        traj = Trajectory(T, n, learner=True)
         entry = {}
-        for K in (16, 1):
+        for K, learner in ((16, False), (1, False), (16, True)):
+            pol = pol_value if learner else pol_plain
             structs = [traj.rows(k0, K) for k0 in range(0, T, K)]
+            if not learner:
+                for st in structs:
+                    st.logp = st.value = None
             times = []
             for r in range(3):
                 start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -337,14 +345,16 @@ def policy_sweep(stream) -> dict:
                 if r:
                     times.append(start.elapsed_time(stop))
             ms = min(times)
-            entry[f"K{K}"] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3),
-                              "mlp_TFLOPs": n * T * MLP_FLOPS_PER_ENV_STEP / (ms * 1e-3) / 1e12}
+            entry[f"K{K}" + ("_learner" if learner else "")] = {
+                "ms": ms, "env_steps_per_s": n * T / (ms * 1e-3),
+                "mlp_TFLOPs": n * T * MLP_FLOPS_PER_ENV_STEP / (ms * 1e-3) / 1e12}
         entry["fusion_speedup"] = entry["K1"]["ms"] / entry["K16"]["ms"]
+        entry["learner_outputs_cost"] = entry["K16_learner"]["ms"] / entry["K16"]["ms"] - 1.0
         rows[dtype] = entry
         del traj
         sim.close()
-        print(f"[bench] policy {dtype}: K16 {entry['K16']['ms']:.2f} ms, K1 {entry['K1']['ms']:.2f} ms",
-              file=sys.stderr, flush=True)
+        print(f"[bench] policy {dtype}: K16 {entry['K16']['ms']:.2f} ms, K1 {entry['K1']['ms']:.2f} ms, "
+              f"K16 + log pi/value {entry['K16_learner']['ms']:.2f} ms", file=sys.stderr, flush=True)
     return rows
 
 

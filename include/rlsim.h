@@ -99,6 +99,13 @@ int rlsim_reset(rlsim_t* h, uint64_t seed);
  *              lengths, terminated, truncated} over this call's K steps
  *   policy_p0  [K][n_envs]    f32  optional; policy runs only: the policy's
  *              probability of action 0 at each step
+ *   logp       [K][n_envs]    f32  optional; policy runs only: log pi(a|obs) of
+ *              the action taken, log softmax(logits)[a]
+ *   value      [K][n_envs]    f32  optional; policy runs with a value head only:
+ *              v(obs) = wv . h2 + bv
+ * logp and value are what an actor-critic learner reads beside the trajectory
+ * (the data-collection loop forms the learner's training data, Background,
+ * "RL Training"); the caller's tensors are the learner's input as they stand.
  * obs, action, reward and done are all set or all NULL (no trajectory). */
 typedef struct {
     float* obs;
@@ -107,18 +114,22 @@ typedef struct {
     uint8_t* done;
     uint32_t* block_stats;
     float* policy_p0;
+    float* logp;
+    float* value;
 } rlsim_traj;
 
 /* Caller-owned DEVICE weights of the MLP policy 4 -> 64 -> 64 -> 2 (tanh hidden
  * layers; the inference half of the simulation/inference loop, fused with the
- * simulator as the paper's Future Work proposes).  Weights are row-major
- * [out][in] in dtype (RLSIM_F32: float, RLSIM_BF16: bfloat16 bits as uint16);
- * biases are always float and may be NULL (zero). */
+ * simulator as the paper's Future Work proposes) and of an optional value head
+ * 64 -> 1 on the second hidden layer h2.  Weights are row-major [out][in] in
+ * dtype (RLSIM_F32: float, RLSIM_BF16: bfloat16 bits as uint16); biases are
+ * always float and may be NULL (zero).  wv NULL = no value head. */
 typedef struct {
     int dtype;
     const void* w1; const float* b1;    /* 64 x 4,  64 */
     const void* w2; const float* b2;    /* 64 x 64, 64 */
     const void* w3; const float* b3;    /* 2 x 64,  2  */
+    const void* wv; const float* bv;    /* 1 x 64,  1  (value head, optional) */
 } rlsim_policy;
 
 /* Run global steps t .. t+K-1 of every environment in exactly one kernel launch
@@ -132,9 +143,10 @@ typedef struct {
  * episode starts from the reset draw of step t+k+1 with zero padding words.
  * policy_or_null: NULL = random actions.  traj_or_null: NULL = record nothing.
  * Errors: EINVAL (h NULL, K == 0, t + K > 2^32 - 1, a mixed set of NULL
- * trajectory pointers, a float pointer not 4-byte aligned, policy_p0 without a
- * policy, a policy with NULL weights or unknown dtype); ESTATE (before
- * rlsim_reset); EUNSUPPORTED (a policy with D > 0); EDEVICE. */
+ * trajectory pointers, a float pointer not 4-byte aligned, policy_p0, logp or
+ * value without a policy, value without wv, a policy with NULL w1/w2/w3 or
+ * unknown dtype); ESTATE (before rlsim_reset); EUNSUPPORTED (a policy with
+ * D > 0); EDEVICE. */
 int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy_or_null,
                      const rlsim_traj* traj_or_null);
 

@@ -4,7 +4,9 @@
 //     h1 = tanh(W1 obs + b1), h2 = tanh(W2 h1 + b2), logits = W3 h2 + b3,
 //     p0 = softmax(logits)[0] = 1 / (1 + exp(l1 - l0)),
 // samples action 0 when u < p0 (u from Philox stream POLICY), then takes the
-// cart-pole step exactly as the random-action kernel does.
+// cart-pole step exactly as the random-action kernel does.  On request it also
+// records what an actor-critic learner reads per step: log pi(a|obs) of the
+// action taken and the value head v = Wv h2 + bv on the same trunk.
 //
 // Matrix layout.  A wave owns 64 environments (lane = environment for the
 // cart-pole state) and runs the MLP as two 32-environment column tiles of the
@@ -16,7 +18,7 @@
 // gathered in that permuted order once per launch, so activations never move
 // between lanes.  The output layer puts logit rows at 0,1 (tile 0) and 4,5
 // (tile 1) so that every lane finds its own environment's logits in its own
-// registers 0 and 1.
+// registers 0 and 1, and the value row at 2 (tile 0) and 6 (tile 1), register 2.
 #pragma once
 
 #include "k_cartpole.hip.h"
@@ -33,8 +35,23 @@ struct PolicyArgs {
     const float* b2;    // [64] or null
     const void* w3;     // [2][64]
     const float* b3;    // [2] or null
+    const void* wv;     // [1][64] value head or null
+    const float* bv;    // [1] or null
     float* p0;          // [K][n] or null
+    float* logp;        // [K][n] or null
+    float* value;       // [K][n] or null
 };
+
+// log pi(a) for two logits, from d = l1 - l0: with z = l_other - l_a,
+// log pi(a) = -softplus(z) = -(max(z, 0) + log(1 + e^-|z|)).  e^-|z| is in
+// (0, 1], so the log term is in [0, ln 2] and neither part can overflow.
+__device__ __forceinline__ float log_pi(float d, uint32_t act)
+{
+    const float z = act ? -d : d;
+    const float e = __builtin_amdgcn_exp2f(-__builtin_fabsf(z) * 1.44269504088896340736f);
+    const float l1p = __builtin_amdgcn_logf(1.0f + e) * 0.69314718055994530942f;
+    return -(__builtin_fmaxf(z, 0.0f) + l1p);
+}
 
 // Hidden unit held by accumulator register i of a lane in half h (0: lanes
 // 0-31, 1: lanes 32-63) of row tile M.
@@ -76,8 +93,8 @@ __device__ __forceinline__ floatx16 bias_tile(const float* lds_b, uint32_t M, ui
 struct MlpBf16 {
     bf16x8 a1[2];        // layer 1, row tiles 0/1; K = obs in k 0-3 and 8-11
     bf16x8 a2[2][4];     // layer 2, [out tile][K step]
-    bf16x8 a3[4];        // layer 3, [K step]; rows 0,1 and 4,5 = the two logits
-    float b3_0, b3_1;
+    bf16x8 a3[4];        // layer 3, [K step]; rows 0,1 and 4,5 = the two logits, 2 and 6 = value
+    float b3_0, b3_1, bv;
 
     // hidden-input unit of K step s, element j, for a lane in half h
     __device__ static uint32_t k_unit(uint32_t s, uint32_t j, uint32_t h)
@@ -100,21 +117,29 @@ struct MlpBf16 {
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
                     a2[Mo][s][j] = to_bf16(weight_at(w.w2, true, (32u * Mo + col) * 64u + k_unit(s, j, h)));
-        const int out = (col == 0u || col == 4u) ? 0 : (col == 1u || col == 5u) ? 1 : -1;
+        const uint32_t r = col % 4u;
+        const bool row_ok = col < 8u && (r < 2u || (r == 2u && w.wv != nullptr));
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                a3[s][j] = to_bf16(out >= 0 ? weight_at(w.w3, true, (uint32_t)out * 64u + k_unit(s, j, h)) : 0.0f);
+                a3[s][j] = to_bf16(!row_ok ? 0.0f
+                                   : r == 2u ? weight_at(w.wv, true, k_unit(s, j, h))
+                                             : weight_at(w.w3, true, r * 64u + k_unit(s, j, h)));
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
+        bv = w.bv ? w.bv[0] : 0.0f;
     }
 
-    // p0 of this lane's environment; obs is this lane's pre-step state.
     static constexpr int kW3 = 1;
     __device__ static void fill_w3(const PolicyArgs&, float*) {}
 
-    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, const float*, uint32_t lane) const
+    // Logit difference d = l1 - l0 and value v of this lane's environment; obs
+    // is this lane's pre-step state.  The value row rides in the output tile at
+    // no extra cost, so VAL changes nothing here.
+    template <bool VAL>
+    __device__ void eval(const CartState& obs, const float* lds_b1, const float* lds_b2, const float*, uint32_t lane,
+                         float& d, float& v) const
     {
         const uint32_t h = lane / 32u;
         const bf16x8 zero8 = {};
@@ -123,7 +148,7 @@ struct MlpBf16 {
         own[1] = to_bf16(obs.xd);
         own[2] = to_bf16(obs.th);
         own[3] = to_bf16(obs.thd);
-        float l0 = 0.0f, l1 = 0.0f;
+        float l0 = 0.0f, l1 = 0.0f, lv = 0.0f;
 #pragma unroll
         for (uint32_t T = 0; T < 2u; ++T) {
             // layer 1: tile T's environments live in half T
@@ -150,20 +175,21 @@ struct MlpBf16 {
             for (int s = 0; s < 4; ++s)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) b2[s][j] = to_bf16(tanh_fast(c2[s / 2][8 * (s % 2) + j]));
-            // layer 3: rows 0,1 (tile 0) / 4,5 (tile 1) are registers 0,1 of the owning half
+            // layer 3: rows 0,1,2 (tile 0) / 4,5,6 (tile 1) are registers 0,1,2 of the owning half
             floatx16 c3 = {};
             c3[0] = b3_0;
             c3[1] = b3_1;
+            c3[2] = bv;
 #pragma unroll
             for (int s = 0; s < 4; ++s) c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[s], b2[s], c3, 0, 0, 0);
             if (h == T) {
                 l0 = c3[0];
                 l1 = c3[1];
+                lv = c3[2];
             }
         }
-        // softmax over two logits
-        const float e = __builtin_amdgcn_exp2f((l1 - l0) * 1.44269504088896340736f);
-        return __builtin_amdgcn_rcpf(1.0f + e);
+        d = l1 - l0;
+        v = lv;
     }
 };
 
@@ -175,16 +201,18 @@ struct MlpBf16 {
 struct MlpF32 {
     float a1[2][4];      // layer 1 [row tile][obs index]; both halves hold the same weight
     float a2[2][2][16];  // layer 2 [out tile][in tile][accumulator register]
-    float b3_0, b3_1;
+    float b3_0, b3_1, bv;
 
-    // Output-layer weights a lane of half h needs, [logit][in tile][half][register]:
-    // W3[o][acc_row(Mi, i, h)]; filled once per workgroup.
-    static constexpr int kW3 = 2 * 2 * 2 * 16;
+    // Output-layer weights a lane of half h needs, [output][in tile][half][register]:
+    // W3[o][acc_row(Mi, i, h)] for the logits o = 0, 1 and Wv[acc_row(Mi, i, h)]
+    // (zero without a value head) as output 2; filled once per workgroup.
+    static constexpr int kW3 = 3 * 2 * 2 * 16;
     __device__ static void fill_w3(const PolicyArgs& w, float* lds_w3)
     {
         for (uint32_t q = threadIdx.x; q < (uint32_t)kW3; q += kBlock) {
             const uint32_t o = q / 64u, Mi = (q / 32u) % 2u, h = (q / 16u) % 2u, i = q % 16u;
-            lds_w3[q] = weight_at(w.w3, false, o * 64u + acc_row(Mi, i, h));
+            lds_w3[q] = o < 2u ? weight_at(w.w3, false, o * 64u + acc_row(Mi, i, h))
+                               : (w.wv ? weight_at(w.wv, false, acc_row(Mi, i, h)) : 0.0f);
         }
     }
 
@@ -204,10 +232,13 @@ struct MlpF32 {
                     a2[Mo][Mi][i] = weight_at(w.w2, false, (32u * Mo + col) * 64u + acc_row(Mi, i, h));
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
+        bv = w.bv ? w.bv[0] : 0.0f;
     }
 
-    __device__ float p0(const CartState& obs, const float* lds_b1, const float* lds_b2, const float* lds_w3,
-                        uint32_t lane) const
+    // Logit difference d = l1 - l0 and (if VAL) value v of this lane's environment.
+    template <bool VAL>
+    __device__ void eval(const CartState& obs, const float* lds_b1, const float* lds_b2, const float* lds_w3,
+                         uint32_t lane, float& d, float& v) const
     {
         const uint32_t h = lane / 32u;
         const float own[4] = {obs.x, obs.xd, obs.th, obs.thd};
@@ -244,18 +275,20 @@ struct MlpF32 {
                     for (int Mo = 0; Mo < 2; ++Mo)
                         c2[T][Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2[Mo][Mi][i], c1[T][Mi][i], c2[T][Mo], 0, 0, 0);
         // layer 3 on the VALU: this lane's half of the hidden units, for both tiles
-        float part[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};   // [tile][logit]
+        float part[2][3] = {{0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f}};   // [tile][logit 0, logit 1, value]
 #pragma unroll
         for (int Mi = 0; Mi < 2; ++Mi)
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const float w0 = lds_w3[(0 * 2 + Mi) * 32 + h * 16 + i];
                 const float w1 = lds_w3[(1 * 2 + Mi) * 32 + h * 16 + i];
+                const float wv = VAL ? lds_w3[(2 * 2 + Mi) * 32 + h * 16 + i] : 0.0f;
 #pragma unroll
                 for (int T = 0; T < 2; ++T) {
-                    const float v = tanh_fast(c2[T][Mi][i]);
-                    part[T][0] = __builtin_fmaf(w0, v, part[T][0]);
-                    part[T][1] = __builtin_fmaf(w1, v, part[T][1]);
+                    const float hv = tanh_fast(c2[T][Mi][i]);
+                    part[T][0] = __builtin_fmaf(w0, hv, part[T][0]);
+                    part[T][1] = __builtin_fmaf(w1, hv, part[T][1]);
+                    if (VAL) part[T][2] = __builtin_fmaf(wv, hv, part[T][2]);
                 }
             }
         // this lane's environment is column lane%32 of tile h; the other half of
@@ -266,15 +299,20 @@ struct MlpF32 {
         const float recv1 = __shfl_xor(send1, 32, 64);
         const float l0 = (h ? part[1][0] : part[0][0]) + recv0 + b3_0;
         const float l1 = (h ? part[1][1] : part[0][1]) + recv1 + b3_1;
-        const float e = __builtin_amdgcn_exp2f((l1 - l0) * 1.44269504088896340736f);
-        return __builtin_amdgcn_rcpf(1.0f + e);
+        d = l1 - l0;
+        v = 0.0f;
+        if (VAL) {
+            const float recv2 = __shfl_xor(h ? part[0][2] : part[1][2], 32, 64);
+            v = (h ? part[1][2] : part[0][2]) + recv2 + bv;
+        }
     }
 };
 
 // Fused policy + cart-pole kernel.  Every lane takes part in the MLP (the
 // matrix instructions need the whole wave); lanes past n_envs carry a zero
-// state and store nothing.
-template <class Mlp, bool REC, bool STATS, bool P0>
+// state and store nothing.  OUT: some of the per-step policy outputs (p0,
+// log pi, value) are recorded; each row pointer may still be null.
+template <class Mlp, bool REC, bool STATS, bool OUT>
 __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs w)
 {
     __shared__ float lds_b1[64];
@@ -306,6 +344,8 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
     }
     if (REC) core.set_rows(a, 0);
     float* p0_row = w.p0;
+    float* lp_row = w.logp;
+    float* v_row = w.value;
     uint4 pw = make_uint4(0u, 0u, 0u, 0u);
     NoPad nopad;
     for (uint32_t k = 0; k < a.K; ++k) {
@@ -313,14 +353,25 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
         if (k == 0u || ((t + 1u) & 7u) == 0u) core.draw_reset((t + 1u) >> 3);
         if (k == 0u || (t & 3u) == 0u) pw = philox(env, t >> 2, STREAM_POLICY, p.key0, p.key1);
         const float u = u24(pick_word(pw, t & 3u));
-        const float p0 = mlp.p0(core.s, lds_b1, lds_b2, lds_w3, lane);
+        float d, v;
+        mlp.template eval<OUT>(core.s, lds_b1, lds_b2, lds_w3, lane, d, v);
+        // softmax over two logits: p0 = 1 / (1 + e^(l1 - l0))
+        const float p0 = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(d * 1.44269504088896340736f));
         const uint32_t act = (u < p0) ? 0u : 1u;
         if (live) {
-            if (P0) *at(p0_row, env * 4u) = p0;
+            if (OUT) {
+                if (p0_row) *at(p0_row, env * 4u) = p0;
+                if (lp_row) *at(lp_row, env * 4u) = log_pi(d, act);
+                if (v_row) *at(v_row, env * 4u) = v;
+            }
             core.step_with(act, nopad);
         }
         // row pointers stay wave-uniform: advanced outside the lane branch
-        if (P0) p0_row += a.n;
+        if (OUT) {
+            if (p0_row) p0_row += a.n;
+            if (lp_row) lp_row += a.n;
+            if (v_row) v_row += a.n;
+        }
         if (REC) core.advance_rows();
     }
     if (live) core.store(a);

@@ -189,7 +189,7 @@ template <class Mlp, bool REC, bool STATS>
 hipError_t launch_policy(const StepArgs& a, const PolicyArgs& w, hipStream_t s)
 {
     const dim3 grid(grid_for(a.n)), block(kBlock);
-    if (w.p0) hipLaunchKernelGGL((k_policy_fused<Mlp, REC, STATS, true>), grid, block, 0, s, a, w);
+    if (w.p0 || w.logp || w.value) hipLaunchKernelGGL((k_policy_fused<Mlp, REC, STATS, true>), grid, block, 0, s, a, w);
     else hipLaunchKernelGGL((k_policy_fused<Mlp, REC, STATS, false>), grid, block, 0, s, a, w);
     return hipGetLastError();
 }
@@ -318,17 +318,21 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     const int n_set = (tr.obs != nullptr) + (tr.action != nullptr) + (tr.reward != nullptr) + (tr.done != nullptr);
     if (n_set != 0 && n_set != 4)
         return fail(h, RLSIM_EINVAL, "rlsim_step_fused: obs, action, reward and done must be all set or all NULL");
-    if (!aligned4(tr.obs) || !aligned4(tr.reward) || !aligned4(tr.block_stats) || !aligned4(tr.policy_p0))
+    if (!aligned4(tr.obs) || !aligned4(tr.reward) || !aligned4(tr.block_stats) || !aligned4(tr.policy_p0) ||
+        !aligned4(tr.logp) || !aligned4(tr.value))
         return fail(h, RLSIM_EINVAL, "rlsim_step_fused: f32/u32 pointers must be 4-byte aligned");
-    if (tr.policy_p0 && !policy) return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy_p0 needs a policy");
+    if ((tr.policy_p0 || tr.logp || tr.value) && !policy)
+        return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy_p0, logp and value need a policy");
     if (policy) {
         if (policy->dtype != RLSIM_F32 && policy->dtype != RLSIM_BF16)
             return fail(h, RLSIM_EINVAL, "rlsim_step_fused: unknown policy dtype");
         if (!policy->w1 || !policy->w2 || !policy->w3)
             return fail(h, RLSIM_EINVAL, "rlsim_step_fused: policy weights must not be NULL");
+        if (tr.value && !policy->wv)
+            return fail(h, RLSIM_EINVAL, "rlsim_step_fused: value output needs the value head wv");
         const size_t wal = policy->dtype == RLSIM_F32 ? 4 : 2;
-        if (((uintptr_t)policy->w1 | (uintptr_t)policy->w2 | (uintptr_t)policy->w3) % wal != 0 ||
-            !aligned4(policy->b1) || !aligned4(policy->b2) || !aligned4(policy->b3))
+        if (((uintptr_t)policy->w1 | (uintptr_t)policy->w2 | (uintptr_t)policy->w3 | (uintptr_t)policy->wv) % wal != 0 ||
+            !aligned4(policy->b1) || !aligned4(policy->b2) || !aligned4(policy->b3) || !aligned4(policy->bv))
             return fail(h, RLSIM_EINVAL, "rlsim_step_fused: misaligned policy arrays");
         if (h->D != 0u)
             return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: a policy with padding words is not supported");
@@ -356,7 +360,8 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
     hipError_t e;
     if (policy) {
-        PolicyArgs w{policy->w1, policy->b1, policy->w2, policy->b2, policy->w3, policy->b3, tr.policy_p0};
+        PolicyArgs w{policy->w1, policy->b1, policy->w2, policy->b2, policy->w3, policy->b3,
+                     policy->wv, policy->bv, tr.policy_p0, tr.logp, tr.value};
         e = policy->dtype == RLSIM_BF16 ? launch_policy_any<MlpBf16>(a, w, rec, stats, h->stream)
                                         : launch_policy_any<MlpF32>(a, w, rec, stats, h->stream);
         if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");

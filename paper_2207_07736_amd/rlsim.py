@@ -52,14 +52,16 @@ class rlsim_cfg(ctypes.Structure):
 
 class rlsim_traj(ctypes.Structure):
     _fields_ = [("obs", ctypes.c_void_p), ("action", ctypes.c_void_p), ("reward", ctypes.c_void_p),
-                ("done", ctypes.c_void_p), ("block_stats", ctypes.c_void_p), ("policy_p0", ctypes.c_void_p)]
+                ("done", ctypes.c_void_p), ("block_stats", ctypes.c_void_p), ("policy_p0", ctypes.c_void_p),
+                ("logp", ctypes.c_void_p), ("value", ctypes.c_void_p)]
 
 
 class rlsim_policy(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int),
                 ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
                 ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
-                ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p)]
+                ("w3", ctypes.c_void_p), ("b3", ctypes.c_void_p),
+                ("wv", ctypes.c_void_p), ("bv", ctypes.c_void_p)]
 
 
 def _load():
@@ -168,20 +170,24 @@ def _ptr(t):
     return None if t is None else t.data_ptr()
 
 
-def traj_struct(obs=None, action=None, reward=None, done=None, block_stats=None, policy_p0=None) -> rlsim_traj:
+def traj_struct(obs=None, action=None, reward=None, done=None, block_stats=None, policy_p0=None,
+                logp=None, value=None) -> rlsim_traj:
     """rlsim_traj from torch tensors (or None)."""
-    return rlsim_traj(_ptr(obs), _ptr(action), _ptr(reward), _ptr(done), _ptr(block_stats), _ptr(policy_p0))
+    return rlsim_traj(_ptr(obs), _ptr(action), _ptr(reward), _ptr(done), _ptr(block_stats), _ptr(policy_p0),
+                      _ptr(logp), _ptr(value))
 
 
-def policy_struct(dtype: int, w1, b1, w2, b2, w3, b3) -> rlsim_policy:
-    """rlsim_policy from device tensors (weights fp32 or bf16, biases fp32 or None)."""
-    return rlsim_policy(int(dtype), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3), _ptr(b3))
+def policy_struct(dtype: int, w1, b1, w2, b2, w3, b3, wv=None, bv=None) -> rlsim_policy:
+    """rlsim_policy from device tensors (weights fp32 or bf16, biases fp32 or
+    None; wv/bv the optional value head)."""
+    return rlsim_policy(int(dtype), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3), _ptr(b3), _ptr(wv), _ptr(bv))
 
 
 class Trajectory:
-    """Device buffers of K trajectory rows for n environments (torch tensors)."""
+    """Device buffers of K trajectory rows for n environments (torch tensors).
+    ``learner=True`` adds the per-step log pi(a|obs) and value planes."""
 
-    def __init__(self, K: int, n: int, device="cuda", stats: bool = True, p0: bool = False):
+    def __init__(self, K: int, n: int, device="cuda", stats: bool = True, p0: bool = False, learner: bool = False):
         import torch
         self.K, self.n = K, n
         self.obs = torch.empty((K, 4, n), dtype=torch.float32, device=device)
@@ -190,14 +196,26 @@ class Trajectory:
         self.done = torch.empty((K, n), dtype=torch.uint8, device=device)
         self.block_stats = torch.empty(((n + 255) // 256, 4), dtype=torch.int32, device=device) if stats else None
         self.policy_p0 = torch.empty((K, n), dtype=torch.float32, device=device) if p0 else None
+        self.logp = torch.empty((K, n), dtype=torch.float32, device=device) if learner else None
+        self.value = torch.empty((K, n), dtype=torch.float32, device=device) if learner else None
 
     def rows(self, k0: int, k: int) -> rlsim_traj:
         """Struct addressing rows k0 .. k0+k-1 (for a call with K = k)."""
         if k0 < 0 or k0 + k > self.K:
             raise ValueError("row range outside the trajectory")
+        part = lambda x: None if x is None else x[k0:k0 + k]  # noqa: E731
         return traj_struct(self.obs[k0:k0 + k], self.action[k0:k0 + k], self.reward[k0:k0 + k],
-                           self.done[k0:k0 + k], self.block_stats,
-                           None if self.policy_p0 is None else self.policy_p0[k0:k0 + k])
+                           self.done[k0:k0 + k], self.block_stats, part(self.policy_p0), part(self.logp),
+                           part(self.value))
+
+    def learner_batch(self) -> dict:
+        """The recorded rows as a learner reads them, as views of the buffers the
+        kernel wrote (no copy): obs [K, n, 4], action, reward, done, and when
+        recorded logp and value [K, n]."""
+        out = dict(obs=self.obs.permute(0, 2, 1), action=self.action, reward=self.reward, done=self.done)
+        if self.logp is not None:
+            out["logp"], out["value"] = self.logp, self.value
+        return out
 
 
 class Simulator:

@@ -160,3 +160,26 @@ def test_create_rejects_zero_compute_factor():
     with pytest.raises(p.RlsimError) as e:
         p.rlsim_create(8, 4, c)
     assert e.value.code == p.RLSIM_EINVAL
+
+
+def test_binding_struct_layouts_match_the_header(tmp_path):
+    """sizeof and every field offset of the three ABI structs, as a C compiler
+    lays them out from include/rlsim.h, equal the ctypes binding's."""
+    import paper_2207_07736_amd as p
+    structs = {"rlsim_cfg": p.rlsim_cfg, "rlsim_traj": p.rlsim_traj, "rlsim_policy": p.rlsim_policy}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "rlsim.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'printf("{name} sizeof %zu\\n", sizeof({name}));')
+        for field, _ in cls._fields_:
+            lines.append(f'printf("{name} {field} %zu\\n", offsetof({name}, {field}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    for row in filter(None, got):
+        name, field, val = row.split()
+        cls = structs[name]
+        want = ctypes.sizeof(cls) if field == "sizeof" else getattr(cls, field).offset
+        assert int(val) == want, row

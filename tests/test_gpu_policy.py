@@ -11,6 +11,12 @@ are:
   step or the reset draw);
 * free-running: an environment's trajectory equals the oracle's up to its first
   action disagreement, which must be one of the exempt ones above.
+
+The learner outputs are compared teacher-forced too, with the GPU's action:
+log pi(a|obs) and the value head within 4 x the p0 tolerance (+1e-6 for the
+log's own evaluation).  p0 = 1/(1 + e^d) with d = l1 - l0 has |dp0/dd| <= 1/4,
+so the p0 tolerance already admits a logit error of 4 x itself; log pi moves
+by at most |d error|, and the value is one such sum.
 """
 import numpy as np
 import pytest
@@ -22,6 +28,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 TOL = {"f32": (1e-5, 1e-4), "bf16": (1e-3, 2e-3)}
+LEARNER_TOL = {k: 4.0 * v[0] + 1e-6 for k, v in TOL.items()}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -35,7 +42,7 @@ def _weights(seed, bias_scale=0.0):
     w = workloads.mlp_weights(seed)
     if bias_scale:
         rng = np.random.Generator(np.random.PCG64(seed + 1))
-        for k in ("b1", "b2", "b3"):
+        for k in ("b1", "b2", "b3", "bv"):
             w[k] = (rng.standard_normal(w[k].shape) * bias_scale).astype(np.float32)
     return w
 
@@ -44,20 +51,22 @@ def _device_policy(w, dtype):
     import paper_2207_07736_amd as p
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     dev = {k: torch.from_numpy(w[k]).to("cuda") for k in w}
-    tens = dict(w1=dev["w1"].to(tdt).contiguous(), w2=dev["w2"].to(tdt).contiguous(), w3=dev["w3"].to(tdt).contiguous(),
-                b1=dev["b1"].contiguous(), b2=dev["b2"].contiguous(), b3=dev["b3"].contiguous())
+    tens = {k: dev[k].to(tdt).contiguous() for k in ("w1", "w2", "w3", "wv") if k in dev}
+    tens.update({k: dev[k].contiguous() for k in ("b1", "b2", "b3", "bv") if k in dev})
     st = p.policy_struct(p.RLSIM_BF16 if dtype == "bf16" else p.RLSIM_F32, tens["w1"], tens["b1"], tens["w2"],
-                         tens["b2"], tens["w3"], tens["b3"])
+                         tens["b2"], tens["w3"], tens["b3"], tens.get("wv"), tens.get("bv"))
     return st, tens
 
 
-def _gpu_policy_run(n, T, K, w, dtype, seed, cfg=None, slices=None):
+def _gpu_policy_run(n, T, K, w, dtype, seed, cfg=None, slices=None, learner=None):
     import paper_2207_07736_amd as p
+    if learner is None:
+        learner = "wv" in w
     st, keep = _device_policy(w, dtype)
     sim = p.Simulator(n, 0, cfg or workloads.CARTPOLE)
     try:
         sim.reset(seed)
-        tr = p.Trajectory(T, n, p0=True)
+        tr = p.Trajectory(T, n, p0=True, learner=learner)
         stats = []
         for k0 in range(0, T, K):
             sim.step(min(K, T - k0), tr.rows(k0, min(K, T - k0)), policy=st)
@@ -71,6 +80,8 @@ def _gpu_policy_run(n, T, K, w, dtype, seed, cfg=None, slices=None):
 
         out = dict(obs=cols(tr.obs), action=cols(tr.action), reward=cols(tr.reward), done=cols(tr.done),
                    p0=cols(tr.policy_p0), stats=[s.cpu().numpy().view(np.uint32) for s in stats])
+        if learner:
+            out["logp"], out["value"] = cols(tr.logp), cols(tr.value)
         state, ep, t = sim.get_state()
         out["t"] = t
         del tr, keep
@@ -84,6 +95,7 @@ def _check_teacher_forced(g, w, dtype, seed, env_ids, cfg=None):
     params = oracle.make_params(**(cfg or workloads.CARTPOLE))
     pol = oracle.Policy(**w, bf16=(dtype == "bf16"))
     p_tol, delta = TOL[dtype]
+    l_tol = LEARNER_TOL[dtype]
     T = g["action"].shape[0]
     worst, exempt = 0.0, 0
     for col, env in enumerate(env_ids):
@@ -93,9 +105,13 @@ def _check_teacher_forced(g, w, dtype, seed, env_ids, cfg=None):
             p_gpu = float(g["p0"][t, col])
             a = int(g["action"][t, col])
             assert a == (0 if u < p_gpu else 1), (env, t, u, p_gpu, a)
-            p_ref = pol.p0(obs)
+            logit, p_ref, v_ref = pol.eval(obs)
             worst = max(worst, abs(p_gpu - p_ref))
             assert abs(p_gpu - p_ref) <= p_tol, (env, t, p_gpu, p_ref)
+            if "logp" in g:
+                lp_ref = oracle.log_prob(logit, a)
+                assert abs(float(g["logp"][t, col]) - lp_ref) <= l_tol, (env, t, g["logp"][t, col], lp_ref)
+                assert abs(float(g["value"][t, col]) - v_ref) <= l_tol, (env, t, g["value"][t, col], v_ref)
             a_ref = 0 if u < p_ref else 1
             if a != a_ref:
                 assert abs(u - p_ref) <= delta, (env, t, u, p_ref)
@@ -160,6 +176,7 @@ def test_policy_zero_weights_is_coin_flip():
     for dtype in ("f32", "bf16"):
         g = _gpu_policy_run(n, T, 8, z, dtype, seed)
         assert np.all(g["p0"] == 0.5)
+        assert np.all(np.abs(g["logp"] + np.log(2.0)) <= 1e-7) and np.all(g["value"] == 0.0)
         sim = oracle.Sim(n, 0, oracle.make_params(**workloads.CARTPOLE))
         sim.reset(seed)
         r = sim.step(T, policy=oracle.Policy(**z))
@@ -182,6 +199,58 @@ def test_c5_full_size_sampled(dtype):
     _check_teacher_forced(gs, wts, dtype, seed, env_ids)
     assert g["t"] == T
     assert np.all(g["reward"] == 1.0) and int(g["action"].max()) <= 1 and int(g["done"].max()) <= 3
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_without_value_head_or_learner_outputs(dtype):
+    """No value head, or no learner planes: p0 and the trajectory are what they
+    are with them (the extra outputs change nothing else)."""
+    n, T, K, seed = 300, 32, 16, 4
+    w = _weights(12, 0.3)
+    full = _gpu_policy_run(n, T, K, w, dtype, seed, learner=True)
+    bare = _gpu_policy_run(n, T, K, w, dtype, seed, learner=False)
+    nov = {k: v for k, v in w.items() if k not in ("wv", "bv")}
+    nohead = _gpu_policy_run(n, T, K, nov, dtype, seed, learner=False)
+    for o in (bare, nohead):
+        for k in ("obs", "action", "done", "p0"):
+            assert np.array_equal(np.asarray(o[k]).view(np.uint8), np.asarray(full[k]).view(np.uint8)), k
+    _check_teacher_forced(full, w, dtype, seed, list(range(n)))
+
+
+def test_learner_batch_is_zero_copy_and_consistent():
+    """The learner reads the kernel's own buffers: views, not copies.  A plain
+    fp32 torch re-evaluation of the policy on those views reproduces the
+    recorded log pi and value (the first-epoch importance ratio of a PPO-style
+    learner is 1)."""
+    import paper_2207_07736_amd as p
+    n, T, K, seed = 4096, 64, 16, 3
+    w = _weights(5, 0.3)
+    st, keep = _device_policy(w, "f32")
+    sim = p.Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(seed)
+        tr = p.Trajectory(T, n, learner=True)
+        for k0 in range(0, T, K):
+            sim.step(K, tr.rows(k0, K), policy=st)
+        torch.cuda.synchronize()
+        b = tr.learner_batch()
+        assert b["obs"].data_ptr() == tr.obs.data_ptr() and b["obs"].shape == (T, n, 4)
+        for k in ("action", "reward", "done", "logp", "value"):
+            assert b[k].data_ptr() == getattr(tr, k).data_ptr()
+        x = b["obs"].reshape(-1, 4)
+        W = {k: torch.from_numpy(w[k]).cuda() for k in w}
+        h = torch.tanh(x @ W["w1"].T + W["b1"])
+        h = torch.tanh(h @ W["w2"].T + W["b2"])
+        logits = h @ W["w3"].T + W["b3"]
+        value = (h @ W["wv"].T + W["bv"])[:, 0]
+        logp = torch.log_softmax(logits, dim=1).gather(1, b["action"].reshape(-1, 1).long())[:, 0]
+        ratio = torch.exp(logp - b["logp"].reshape(-1))
+        assert float((ratio - 1).abs().max()) < 1e-4
+        assert float((value - b["value"].reshape(-1)).abs().max()) < 1e-4
+        del tr, b
+    finally:
+        sim.close()
+    del keep
 
 
 def test_policy_errors():
@@ -207,6 +276,21 @@ def test_policy_errors():
         with pytest.raises(p.RlsimError) as e:
             sim.step(4, None, policy=bad)
         assert e.value.code == p.RLSIM_EINVAL
+        tr = p.Trajectory(4, 100, learner=True)
+        with pytest.raises(p.RlsimError) as e:                     # learner planes without a policy
+            sim.step(4, tr.rows(0, 4))
+        assert e.value.code == p.RLSIM_EINVAL
+        nohead = p.rlsim_policy(p.RLSIM_F32, st.w1, st.b1, st.w2, st.b2, st.w3, st.b3, None, None)
+        with pytest.raises(p.RlsimError) as e:                     # value plane without a value head
+            sim.step(4, tr.rows(0, 4), policy=nohead)
+        assert e.value.code == p.RLSIM_EINVAL
+        mis = p.rlsim_policy(p.RLSIM_F32, st.w1, st.b1, st.w2, st.b2, st.w3, st.b3, st.wv + 2, st.bv)
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(4, None, policy=mis)
+        assert e.value.code == p.RLSIM_EINVAL
+        sim.step(4, tr.rows(0, 4), policy=st)                      # the handle still works
+        torch.cuda.synchronize()
+        del tr
     finally:
         sim.close()
     del keep
