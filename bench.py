@@ -122,25 +122,51 @@ hbm_bytes_per_launch: {hbm:.0f}
     return path
 
 
-def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
-    """The oracle (single-threaded C loop, as it stands) on a bounded sample of
-    the headline workload: `slices` env slices of the 4M batch, T steps each."""
+def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int) -> float:
+    """Wall seconds for the oracle to run T recorded steps of each env slice
+    [start, start + n_slice_envs), `threads` slices at a time.  Each slice is
+    its own oracle instance; the oracle's C loop runs outside the GIL."""
+    import concurrent.futures as cf
+
     import oracle
     params = oracle.make_params(**workloads.CARTPOLE)
-    n_total = workloads.WORKLOADS["C3"]["n"]
-    stride = n_total // slices
-    elapsed = 0.0
-    for i in range(slices):
-        sim = oracle.Sim(n_slice_envs, 0, params, env0=i * stride)
+
+    def one(start):
+        sim = oracle.Sim(n_slice_envs, 0, params, env0=start)
         sim.reset(seed)
         t0 = time.perf_counter()
         sim.step(T)
-        elapsed += time.perf_counter() - t0
-        del sim
-    env_steps = n_slice_envs * slices * T
-    return {"value": env_steps / elapsed, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps of the 4,194,304-env headline batch "
-                      f"(seed {seed}, trajectory recorded), {elapsed:.1f} s"}
+        return time.perf_counter() - t0
+
+    if threads == 1:
+        return sum(one(s) for s in starts)
+    t0 = time.perf_counter()
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(one, starts))
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
+    """The oracle (plain C loop, as it stands) on bounded samples of the
+    headline workload: env slices of the 4M batch, T steps each, trajectory
+    recorded.  Reported multi-threaded (one slice per host thread at a time, as
+    the paper's multi-core C++ simulator baseline divides environments over
+    cores) and single-threaded."""
+    import oracle  # noqa: F401  (builds the oracle before any timing)
+    n_total = workloads.WORKLOADS["C3"]["n"]
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    single_starts = [i * (n_total // slices) for i in range(slices)]
+    single_s = _oracle_slices(n_slice_envs, single_starts, T, seed, 1)
+    single = n_slice_envs * slices * T / single_s
+    mt_slices = 2 * threads
+    mt_starts = [i * (n_total // mt_slices) for i in range(mt_slices)]
+    mt_s = _oracle_slices(n_slice_envs, mt_starts, T, seed, threads)
+    multi = n_slice_envs * mt_slices * T / mt_s
+    return {"value": multi, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{mt_slices} slices x {n_slice_envs} envs x {T} steps of the 4,194,304-env headline batch "
+                      f"(seed {seed}, trajectory recorded) on {threads} threads, {mt_s:.1f} s wall",
+            "single_thread": {"value": single, "unit": "env-steps/s", "cores": 1,
+                              "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps, {single_s:.1f} s"}}
 
 
 def _time_schedule(sim, traj, sched, stream, reps):
@@ -476,6 +502,23 @@ def main() -> int:
                             "speedup": unfused_ms / ms_per_step,
                             "speedup_over_hipgraph": graph_ms / ms_per_step,
                             "unfused_algorithmic_GBs": (n * T * (workloads.TRAJ_BYTES_PER_ENV_STEP + 40)) / (unfused_ms * 1e-3) / 1e9}
+
+    # the store ceiling: the same trajectory bytes, layout and launch shape with
+    # the simulation taken out (librlsim_probe.so), timed like the headline
+    from paper_2207_07736_amd.probe import probe_store
+    for _ in range(2):
+        probe_store(n, K, traj.obs, traj.action, traj.reward, traj.done, stream)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        probe_store(n, K, traj.obs, traj.action, traj.reward, traj.done, stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    probe_ms = start.elapsed_time(stop) / args.steps
+    traj_bytes = n * T * workloads.TRAJ_BYTES_PER_ENV_STEP
+    result["roofline"]["store_probe"] = {
+        "ms": probe_ms, "GBs": traj_bytes / (probe_ms * 1e-3) / 1e9,
+        "frac_of_store_ceiling": (traj_bytes / ms_per_step) / (traj_bytes / probe_ms)}
 
     del traj
     sim.close()

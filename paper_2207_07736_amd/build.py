@@ -1,4 +1,5 @@
-"""Build librlsim.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build librlsim.so (the HIP kernels and the C ABI) and librlsim_probe.so (the
+store-only probe the bench measures the store ceiling with) for gfx950 with hipcc.
 
 Floating-point flags matter for the results: no contraction of a*b+c into an
 FMA unless written, IEEE single-precision division, denormals kept, and no
@@ -14,6 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "rlsim.hip")
 LIB = os.path.join(HERE, "librlsim.so")
+PROBE_SRC = os.path.join(HERE, "csrc", "store_probe.hip")
+PROBE_LIB = os.path.join(HERE, "librlsim_probe.so")
 INCLUDE = os.path.join(ROOT, "include")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,9 +43,16 @@ def sources():
 
 
 def build(verbose: bool = False) -> str:
-    """Compile csrc/rlsim.hip into librlsim.so next to this file (always)."""
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-o", tmp, SRC]
+    """Compile csrc/rlsim.hip into librlsim.so and csrc/store_probe.hip into
+    librlsim_probe.so next to this file (always).  Returns the main library."""
+    _compile(SRC, LIB, verbose)
+    _compile(PROBE_SRC, PROBE_LIB, verbose)
+    return LIB
+
+
+def _compile(src: str, lib: str, verbose: bool) -> None:
+    tmp = lib + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-o", tmp, src]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -53,8 +63,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 def asm(out_path: str) -> str:

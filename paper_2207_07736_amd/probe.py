@@ -1,0 +1,37 @@
+"""Thin ctypes binding of librlsim_probe.so (include/rlsim_probe.h): the
+store-only probe of the trajectory layout, a measurement aid.  Argument
+marshalling only; fails loudly if the library has not been built."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
+PROBE_EXPORTS = ("rlsim_probe_store",)
+
+
+def _load():
+    if not os.path.exists(PROBE_LIB_PATH):
+        raise ImportError(f"{PROBE_LIB_PATH} is missing: build it with paper_2207_07736_amd/build.py")
+    L = ctypes.CDLL(PROBE_LIB_PATH)
+    u32, vp = ctypes.c_uint32, ctypes.c_void_p
+    L.rlsim_probe_store.argtypes = [u32, u32, vp, vp, vp, vp, vp]
+    L.rlsim_probe_store.restype = ctypes.c_int
+    return L
+
+
+probe_lib = _load()
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def probe_store(n: int, K: int, obs, action, reward, done, stream=None) -> None:
+    """Write K trajectory rows for n envs (torch tensors laid out as rlsim_traj)
+    with no simulation; raises ValueError on a rejected argument."""
+    s = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    rc = probe_lib.rlsim_probe_store(int(n), int(K), _ptr(obs), _ptr(action), _ptr(reward), _ptr(done), s)
+    if rc != 0:
+        raise ValueError(f"rlsim_probe_store rejected its arguments (status {rc})")

@@ -183,3 +183,21 @@ def test_binding_struct_layouts_match_the_header(tmp_path):
         cls = structs[name]
         want = ctypes.sizeof(cls) if field == "sizeof" else getattr(cls, field).offset
         assert int(val) == want, row
+
+
+def test_probe_library_exports_and_rejects_bad_arguments():
+    from paper_2207_07736_amd import probe
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "rlsim_probe.h")).read(), flags=re.S)
+    declared = set(re.findall(r"\b(rlsim_[a-z_]+)\s*\(", text))
+    assert declared == set(probe.PROBE_EXPORTS)
+    nm = subprocess.run(["nm", "-D", "--defined-only", probe.PROBE_LIB_PATH], capture_output=True, text=True,
+                        check=True).stdout
+    assert set(re.findall(r" T (rlsim_\w+)", nm)) == declared
+    L = probe.probe_lib
+    # rejected before any device call
+    assert L.rlsim_probe_store(0, 4, 4, 4, 4, 4, None) == -1
+    assert L.rlsim_probe_store(8, 0, 4, 4, 4, 4, None) == -1
+    assert L.rlsim_probe_store(8, 1 << 23, 4, 4, 4, 4, None) == -1
+    assert L.rlsim_probe_store((1 << 30) + 1, 4, 4, 4, 4, 4, None) == -1
+    assert L.rlsim_probe_store(8, 4, None, 4, 4, 4, None) == -1
+    assert L.rlsim_probe_store(8, 4, 6, 4, 4, 4, None) == -1     # misaligned obs

@@ -1,0 +1,59 @@
+"""The store-only probe (include/rlsim_probe.h) writes every byte it claims,
+in the trajectory layout, at a ragged size and at the headline size the bench
+times it at (4,194,304 envs x 200 rows), checked in full on the device."""
+import pytest
+
+import workloads
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _expected_ok(tr, n, K):
+    e = torch.arange(n, device="cuda", dtype=torch.int64)
+    k = torch.arange(K, device="cuda", dtype=torch.int64)[:, None]
+    base = ((e & 0xFFFF)[None, :] + k).to(torch.float32)              # [K][n], exact
+    for c in range(4):
+        if not torch.equal(tr.obs[:, c, :], base + float(c)):
+            return f"obs component {c}"
+    if not torch.equal(tr.action, ((e[None, :] + k) & 1).to(torch.uint8)):
+        return "action"
+    if not bool((tr.reward == 1.0).all()):
+        return "reward"
+    if not torch.equal(tr.done, ((e[None, :] ^ k) & 3).to(torch.uint8)):
+        return "done"
+    return None
+
+
+@pytest.mark.parametrize("n,K", [(1, 3), (1000, 7), (70000, 33)])
+def test_probe_values_ragged(n, K):
+    from paper_2207_07736_amd import Trajectory
+    from paper_2207_07736_amd.probe import probe_store
+    tr = Trajectory(K, n, stats=False)
+    for t in (tr.obs, tr.reward):
+        t.fill_(float("nan"))
+    tr.action.fill_(7)
+    tr.done.fill_(7)
+    probe_store(n, K, tr.obs, tr.action, tr.reward, tr.done)
+    torch.cuda.synchronize()
+    assert _expected_ok(tr, n, K) is None
+
+
+def test_probe_headline_size():
+    from paper_2207_07736_amd import Trajectory
+    from paper_2207_07736_amd.probe import probe_store
+    w = workloads.WORKLOADS["C3"]
+    n, K = w["n"], w["T"]
+    tr = Trajectory(K, n, stats=False)
+    tr.done.fill_(9)
+    s = torch.cuda.Stream()
+    probe_store(n, K, tr.obs, tr.action, tr.reward, tr.done, stream=s)
+    torch.cuda.synchronize()
+    assert _expected_ok(tr, n, K) is None
+    del tr
