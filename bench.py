@@ -26,6 +26,12 @@ import workloads  # noqa: E402
 
 METRIC = "env-steps/sec at 1 MI355X; achieved HBM GB/s vs peak; fused/unfused speedup"
 HBM_PEAK_GBS = 8000.0
+# fp32 VALU peak in lane operations (one FMA or multiply per lane) per second:
+# the published 157.3 TFLOP/s fp32 vector rate counts an FMA as two flops.
+# Plain (non-packed) v_fma_f32 / v_mul_f32 reach it on this part: a
+# store-free chain benchmark measured 5.6e13 / 6.5e13 lane-ops/s at 8 waves
+# per SIMD, above the 3.9e13 a four-cycle wave64 issue would allow.
+VALU_LANE_OPS_PER_S = 157.3e12 / 2
 COPY_BYTES = 1 << 30        # size of the plain copy used to calibrate the HBM byte counters
 
 
@@ -254,6 +260,8 @@ def fusion_sweeps(stream) -> dict:
         ms_nt = _time_schedule(sim, None, [T], stream, reps=2)
         entry["K500_no_trajectory"] = {"ms": ms_nt, "env_steps_per_s": n * T / (ms_nt * 1e-3)}
         entry["fusion_speedup"] = entry["K1"]["ms"] / entry["K500"]["ms"]
+        # fused: one fp32 VALU instruction per padding word per step is the floor
+        entry["K500"]["valu_frac"] = n * D * T / (entry["K500"]["ms"] * 1e-3) / VALU_LANE_OPS_PER_S
         d_rows[f"D{D}"] = entry
         del traj
         sim.close()
@@ -331,6 +339,38 @@ def policy_only(dtype: str, steps: int, warmup: int) -> int:
     return 0
 
 
+def wide_only(D: int, steps: int, warmup: int) -> int:
+    """Timed K = 500 launches of the state-size workload alone (for profiling):
+    262,144 envs x 500 steps with D padding words, trajectory recorded."""
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C4"]
+    n, T = w["n"], w["T"]
+    stream = torch.cuda.current_stream()
+    sim = Simulator(n, D, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    rows = traj.rows(0, T)
+    for _ in range(warmup):
+        sim.step(T, rows)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        sim.step(T, rows)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    updates = n * D * T
+    print(json.dumps({"workload": w["name"], "D": D, "K": T, "ms_per_launch": ms,
+                      "env_steps_per_s": n * T / (ms * 1e-3),
+                      "padding_updates_per_s": updates / (ms * 1e-3),
+                      "valu_frac": updates / (ms * 1e-3) / VALU_LANE_OPS_PER_S}), flush=True)
+    del traj
+    sim.close()
+    return 0
+
+
 def policy_sweep(stream) -> dict:
     """The MLP-policy workload: 1,048,576 envs x 256 steps, fused K = 16 against
     unfused K = 1, fp32 and bf16 weights ~ N(0, 1/fan_in), zero biases; and K =
@@ -398,12 +438,16 @@ def main() -> int:
                     help="also run one plain device copy of 1 GiB (HBM counter calibration)")
     ap.add_argument("--policy", choices=("f32", "bf16"),
                     help="time only the MLP-policy workload (K = 16 launches) in this precision")
+    ap.add_argument("--wide", type=int, metavar="D",
+                    help="time only the state-size workload (262,144 envs, K = 500) with D padding words")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM traffic summary from two rocprofv3 counter CSVs and exit")
     args = ap.parse_args()
 
     if args.policy:
         return policy_only(args.policy, args.steps, args.warmup)
+    if args.wide:
+        return wide_only(args.wide, args.steps, args.warmup)
 
     if args.ingest_pmc:
         w = workloads.WORKLOADS["C3"]
