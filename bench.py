@@ -128,7 +128,7 @@ hbm_bytes_per_launch: {hbm:.0f}
     return path
 
 
-def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int) -> float:
+def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int, D: int = 0, policy=None) -> float:
     """Wall seconds for the oracle to run T recorded steps of each env slice
     [start, start + n_slice_envs), `threads` slices at a time.  Each slice is
     its own oracle instance; the oracle's C loop runs outside the GIL."""
@@ -138,10 +138,10 @@ def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int) -
     params = oracle.make_params(**workloads.CARTPOLE)
 
     def one(start):
-        sim = oracle.Sim(n_slice_envs, 0, params, env0=start)
+        sim = oracle.Sim(n_slice_envs, D, params, env0=start)
         sim.reset(seed)
         t0 = time.perf_counter()
-        sim.step(T)
+        sim.step(T, policy=policy)
         return time.perf_counter() - t0
 
     if threads == 1:
@@ -172,7 +172,36 @@ def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
             "sample": f"{mt_slices} slices x {n_slice_envs} envs x {T} steps of the 4,194,304-env headline batch "
                       f"(seed {seed}, trajectory recorded) on {threads} threads, {mt_s:.1f} s wall",
             "single_thread": {"value": single, "unit": "env-steps/s", "cores": 1,
-                              "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps, {single_s:.1f} s"}}
+                              "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps, {single_s:.1f} s"},
+            "other_workloads": cpu_other_workloads(threads)}
+
+
+def cpu_other_workloads(threads: int) -> dict:
+    """The oracle on bounded slices of the state-size and policy workloads, one
+    slice per thread at a time (env-steps/s; trajectories recorded)."""
+    import oracle
+    out = {}
+    w = workloads.WORKLOADS["C4"]
+    rows = {}
+    for D in w["D"]:
+        n_total = max(4096, min(65536, (1 << 24) // D))       # about 1-3 s of oracle work per D
+        n_slice = n_total // threads
+        starts = [i * (w["n"] // threads) for i in range(threads)]
+        sec = _oracle_slices(n_slice, starts, w["T"], w["seed"], threads, D=D)
+        rows[f"D{D}"] = {"value": n_slice * threads * w["T"] / sec, "unit": "env-steps/s",
+                         "sample": f"{threads} slices x {n_slice} envs x {w['T']} steps, {sec:.1f} s wall"}
+    out[w["name"]] = rows
+    w = workloads.WORKLOADS["C5"]
+    rows = {}
+    for dtype, n_total, T in (("f32", 16384, w["T"]), ("bf16", 4096, 64)):
+        pol = oracle.Policy(**workloads.mlp_weights(w["seed"]), bf16=(dtype == "bf16"))
+        n_slice = n_total // threads
+        starts = [i * (w["n"] // threads) for i in range(threads)]
+        sec = _oracle_slices(n_slice, starts, T, w["seed"], threads, policy=pol)
+        rows[dtype] = {"value": n_slice * threads * T / sec, "unit": "env-steps/s",
+                       "sample": f"{threads} slices x {n_slice} envs x {T} steps (policy, value head), {sec:.1f} s wall"}
+    out[w["name"]] = rows
+    return out
 
 
 def _time_schedule(sim, traj, sched, stream, reps):

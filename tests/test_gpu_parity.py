@@ -251,3 +251,39 @@ def test_compute_factor_bit_exact(C):
     assert_bit_equal(g, r)
     for a, b in zip(g["stats"], r["stats"]):
         assert np.array_equal(a, b)
+
+
+def test_max_envs_sampled():
+    """The largest handle the ABI allows, 2^30 environments, 2 steps in one launch
+    with trajectory and statistics: sampled env slices (first, middle, last) equal
+    the oracle bit for bit, including the byte offsets near 2^32 of the last envs."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    torch.cuda.empty_cache()
+    n, T = 1 << 30, 2
+    slices = [(0, 256), (1 << 29, (1 << 29) + 256), (n - 512, n)]
+    sim = Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(7)
+        traj = Trajectory(T, n)
+        sim.step(T, traj.rows(0, T))
+        torch.cuda.synchronize()
+        cols = lambda x: np.concatenate([x[..., a:b].cpu().numpy() for a, b in slices], axis=-1)  # noqa: E731
+        g = dict(obs=cols(traj.obs), action=cols(traj.action), reward=cols(traj.reward), done=cols(traj.done))
+        blocks = [0, (1 << 29) // 256, n // 256 - 2, n // 256 - 1]
+        g_stats = traj.block_stats[blocks].cpu().numpy().view(np.uint32)
+        del traj
+        state, ep, t = sim.get_state()
+        g["state"] = np.concatenate([state[:, a:b] for a, b in slices], axis=1)
+        g["ep"] = np.concatenate([ep[a:b] for a, b in slices])
+        g["t"] = t
+        del state, ep
+    finally:
+        sim.close()
+        torch.cuda.empty_cache()
+    ref = [oracle_run(b - a, T, [T], seed=7, env0=a) for a, b in slices]
+    merged = {key: np.concatenate([x[key] for x in ref], axis=-1) for key in ("obs", "action", "reward", "done", "state")}
+    merged["ep"] = np.concatenate([x["ep"] for x in ref])
+    merged["t"] = T
+    assert_bit_equal(g, merged)
+    want = np.concatenate([ref[0]["stats"][0], ref[1]["stats"][0], ref[2]["stats"][0]])
+    assert np.array_equal(g_stats, want)
