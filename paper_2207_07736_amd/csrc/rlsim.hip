@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "k_policy.hip.h"
+#include "k_wide.hip.h"
 
 using namespace rlsim_dev;
 
