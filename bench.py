@@ -251,10 +251,25 @@ def _graph_ms(sim, structs, stream, reps: int) -> float:
 
 
 def fusion_sweeps(stream) -> dict:
-    """Fused versus unfused on the K sweep (65,536 envs x 1,000 steps) and the
+    """The 1,024-env correctness workload's launch-bound timing, and fused
+    versus unfused on the K sweep (65,536 envs x 1,000 steps) and the
     state-size sweep (262,144 envs x 500 steps, D padding words per env)."""
     from paper_2207_07736_amd import Simulator, Trajectory
     out = {}
+    w = workloads.WORKLOADS["C1"]
+    n, T = w["n"], w["T"]
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    ms = _time_schedule(sim, traj, [1] * T, stream, reps=5)
+    gms = _graph_ms(sim, [traj.rows(k, 1) for k in range(T)], stream, reps=5)
+    fused = _time_schedule(sim, traj, [T], stream, reps=5)
+    # launch-latency bound: time per launch, not a roofline fraction
+    out[w["name"]] = {"K1": {"ms": ms, "us_per_launch": ms * 1e3 / T},
+                      "K1_hipgraph": {"ms": gms, "us_per_launch": gms * 1e3 / T},
+                      "K100": {"ms": fused}}
+    del traj
+    sim.close()
     w = workloads.WORKLOADS["C2"]
     n, T = w["n"], w["T"]
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
