@@ -131,8 +131,8 @@ struct MlpBf16 {
         bv = w.bv ? w.bv[0] : 0.0f;
     }
 
-    static constexpr int kW3 = 1;
-    __device__ static void fill_w3(const PolicyArgs&, float*) {}
+    static constexpr int kLds = 1;
+    __device__ static void fill_lds(const PolicyArgs&, float*) {}
 
     // Logit difference d = l1 - l0 and value v of this lane's environment; obs
     // is this lane's pre-step state.  The value row rides in the output tile at
@@ -200,36 +200,40 @@ struct MlpBf16 {
 // ---------------------------------------------------------------------------
 struct MlpF32 {
     float a1[2][4];      // layer 1 [row tile][obs index]; both halves hold the same weight
-    float a2[2][2][16];  // layer 2 [out tile][in tile][accumulator register]
     float b3_0, b3_1, bv;
 
-    // Output-layer weights a lane of half h needs, [output][in tile][half][register]:
-    // W3[o][acc_row(Mi, i, h)] for the logits o = 0, 1 and Wv[acc_row(Mi, i, h)]
-    // (zero without a value head) as output 2; filled once per workgroup.
+    // LDS, filled once per workgroup:
+    //  [0, 192): output-layer weights a lane of half h needs, [output][in tile][half][register]:
+    //      W3[o][acc_row(Mi, i, h)] for the logits o = 0, 1 and Wv[acc_row(Mi, i, h)]
+    //      (zero without a value head) as output 2;
+    //  [192, 192 + 4096): layer-2 A operands, float4 (Mo, Mi, i/4, lane) holding
+    //      W2[32 Mo + lane%32][acc_row(Mi, i, lane/32)] for i%4 = 0..3, so that a
+    //      wave reads 1 KB of consecutive float4s per four matrix instructions
+    //      (kept out of registers: 64 fewer VGPRs, one more wave per SIMD).
     static constexpr int kW3 = 3 * 2 * 2 * 16;
-    __device__ static void fill_w3(const PolicyArgs& w, float* lds_w3)
+    static constexpr int kW2 = 2 * 2 * 16 * 64;
+    static constexpr int kLds = kW3 + kW2;
+    __device__ static void fill_lds(const PolicyArgs& w, float* lds)
     {
         for (uint32_t q = threadIdx.x; q < (uint32_t)kW3; q += kBlock) {
             const uint32_t o = q / 64u, Mi = (q / 32u) % 2u, h = (q / 16u) % 2u, i = q % 16u;
-            lds_w3[q] = o < 2u ? weight_at(w.w3, false, o * 64u + acc_row(Mi, i, h))
-                               : (w.wv ? weight_at(w.wv, false, acc_row(Mi, i, h)) : 0.0f);
+            lds[q] = o < 2u ? weight_at(w.w3, false, o * 64u + acc_row(Mi, i, h))
+                            : (w.wv ? weight_at(w.wv, false, acc_row(Mi, i, h)) : 0.0f);
+        }
+        for (uint32_t q = threadIdx.x; q < (uint32_t)kW2; q += kBlock) {
+            const uint32_t r = q % 4u, lane = (q / 4u) % 64u, i4 = (q / 256u) % 4u, Mi = (q / 1024u) % 2u,
+                           Mo = q / 2048u;
+            lds[kW3 + q] = weight_at(w.w2, false, (32u * Mo + lane % 32u) * 64u + acc_row(Mi, 4u * i4 + r, lane / 32u));
         }
     }
 
     __device__ void load(const PolicyArgs& w, uint32_t lane)
     {
-        const uint32_t h = lane / 32u, col = lane % 32u;
+        const uint32_t col = lane % 32u;
 #pragma unroll
         for (int M = 0; M < 2; ++M)
 #pragma unroll
             for (int s = 0; s < 4; ++s) a1[M][s] = weight_at(w.w1, false, (32u * M + col) * 4u + s);
-#pragma unroll
-        for (int Mo = 0; Mo < 2; ++Mo)
-#pragma unroll
-            for (int Mi = 0; Mi < 2; ++Mi)
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    a2[Mo][Mi][i] = weight_at(w.w2, false, (32u * Mo + col) * 64u + acc_row(Mi, i, h));
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
         bv = w.bv ? w.bv[0] : 0.0f;
@@ -265,15 +269,26 @@ struct MlpF32 {
         for (int T = 0; T < 2; ++T)
 #pragma unroll
             for (int Mo = 0; Mo < 2; ++Mo) c2[T][Mo] = bias_tile(lds_b2, Mo, h);
+        const float4* lds_a2 = reinterpret_cast<const float4*>(lds_w3 + kW3);
 #pragma unroll
         for (int Mi = 0; Mi < 2; ++Mi)
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
+            for (int i4 = 0; i4 < 4; ++i4) {
+                float4 w4[2];
 #pragma unroll
-                for (int T = 0; T < 2; ++T)
+                for (int Mo = 0; Mo < 2; ++Mo) w4[Mo] = lds_a2[((Mo * 2 + Mi) * 4 + i4) * 64 + lane];
 #pragma unroll
-                    for (int Mo = 0; Mo < 2; ++Mo)
-                        c2[T][Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2[Mo][Mi][i], c1[T][Mi][i], c2[T][Mo], 0, 0, 0);
+                for (int r = 0; r < 4; ++r) {
+                    const int i = 4 * i4 + r;
+#pragma unroll
+                    for (int T = 0; T < 2; ++T)
+#pragma unroll
+                        for (int Mo = 0; Mo < 2; ++Mo) {
+                            const float a = r == 0 ? w4[Mo].x : r == 1 ? w4[Mo].y : r == 2 ? w4[Mo].z : w4[Mo].w;
+                            c2[T][Mo] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, c1[T][Mi][i], c2[T][Mo], 0, 0, 0);
+                        }
+                }
+            }
         // layer 3 on the VALU: this lane's half of the hidden units, for both tiles
         float part[2][3] = {{0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f}};   // [tile][logit 0, logit 1, value]
 #pragma unroll
@@ -317,12 +332,12 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
 {
     __shared__ float lds_b1[64];
     __shared__ float lds_b2[64];
-    __shared__ float lds_w3[Mlp::kW3];
+    __shared__ __align__(16) float lds_w3[Mlp::kLds];
     if (threadIdx.x < 64u) {
         lds_b1[threadIdx.x] = w.b1 ? w.b1[threadIdx.x] : 0.0f;
         lds_b2[threadIdx.x] = w.b2 ? w.b2[threadIdx.x] : 0.0f;
     }
-    Mlp::fill_w3(w, lds_w3);
+    Mlp::fill_lds(w, lds_w3);
     __syncthreads();
 
     const uint32_t blk = xcd_block();
