@@ -96,43 +96,76 @@ struct MlpBf16 {
     bf16x8 a3[4];        // layer 3, [K step]; rows 0,1 and 4,5 = the two logits, 2 and 6 = value
     float b3_0, b3_1, bv;
 
-    // hidden-input unit of K step s, element j, for a lane in half h
-    __device__ static uint32_t k_unit(uint32_t s, uint32_t j, uint32_t h)
+    // The lanes' operand vectors, staged once per workgroup in LDS as bfloat16
+    // bits, [table][lane][8]: A1 [M 2][64] (obs weights in elements 0-3, zeros
+    // in 4-7), A2 [Mo 2][s 4][64], A3 [s 4][64] (rows 0,1 / 4,5 the logits, 2 / 6
+    // the value, per half).  The fill reads the weights in row-major order, so
+    // global loads are coalesced, and scatters each to its permuted slot; each
+    // lane then reads 14 contiguous 16-byte vectors.
+    static constexpr uint32_t kA1 = 0, kA2 = 2 * 64, kA3 = kA2 + 8 * 64, kVecs = kA3 + 4 * 64;
+    static constexpr int kLds = (int)kVecs * 4;   // floats: 16 B per vector
+
+    // Layers 2 and 3 run over K steps s = 0..3 of 16 hidden units; element j of
+    // step s, for a lane in half h, is hidden unit acc_row(s / 2, 8 (s % 2) + j, h),
+    // the unit that lane holds in its previous layer's accumulator.  unit_slot
+    // inverts that map: the (s, j, h) that reads hidden unit c.
+    __device__ static void unit_slot(uint32_t c, uint32_t& s, uint32_t& j, uint32_t& h)
     {
-        return acc_row(s / 2u, 8u * (s % 2u) + j, h);
+        const uint32_t M = c / 32u, rem = c % 32u;
+        const uint32_t i = 4u * (rem / 8u) + rem % 4u;
+        h = (rem % 8u) / 4u;
+        s = 2u * M + i / 8u;
+        j = i % 8u;
     }
 
-    __device__ void load(const PolicyArgs& w, uint32_t lane)
+    __device__ static void fill_lds(const PolicyArgs& w, float* lds)
     {
-        const uint32_t h = lane / 32u, col = lane % 32u;
+        uint16_t* t = reinterpret_cast<uint16_t*>(lds);
+        uint32_t* t32 = reinterpret_cast<uint32_t*>(lds);
+        for (uint32_t q = threadIdx.x; q < kVecs * 4u; q += kBlock) t32[q] = 0u;
+        __syncthreads();
+        const uint16_t* w1 = reinterpret_cast<const uint16_t*>(w.w1);
+        const uint16_t* w2 = reinterpret_cast<const uint16_t*>(w.w2);
+        const uint16_t* w3 = reinterpret_cast<const uint16_t*>(w.w3);
+        const uint16_t* wv = reinterpret_cast<const uint16_t*>(w.wv);
+        for (uint32_t q = threadIdx.x; q < 64u * 4u; q += kBlock) {          // W1 [64][4]
+            const uint32_t r = q / 4u, c = q % 4u, M = r / 32u, col = r % 32u;
+            const uint16_t v = w1[q];
+            t[((kA1 + M * 64u + col) * 8u) + c] = v;
+            t[((kA1 + M * 64u + 32u + col) * 8u) + c] = v;
+        }
+        for (uint32_t q = threadIdx.x; q < 64u * 64u; q += kBlock) {         // W2 [64][64]
+            const uint32_t r = q / 64u, Mo = r / 32u, col = r % 32u;
+            uint32_t s, j, h;
+            unit_slot(q % 64u, s, j, h);
+            t[(kA2 + (Mo * 4u + s) * 64u + 32u * h + col) * 8u + j] = w2[q];
+        }
+        for (uint32_t q = threadIdx.x; q < 3u * 64u; q += kBlock) {          // W3 [2][64], Wv [64]
+            const uint32_t o = q / 64u;
+            if (o == 2u && wv == nullptr) continue;
+            const uint16_t v = o < 2u ? w3[q] : wv[q % 64u];
+            uint32_t s, j, h;
+            unit_slot(q % 64u, s, j, h);
+            t[(kA3 + s * 64u + 32u * h + o) * 8u + j] = v;
+            t[(kA3 + s * 64u + 32u * h + 4u + o) * 8u + j] = v;
+        }
+    }
+
+    __device__ void load(const PolicyArgs& w, uint32_t lane, const float* lds)
+    {
+        const bf16x8* T = reinterpret_cast<const bf16x8*>(lds);
 #pragma unroll
-        for (int M = 0; M < 2; ++M)
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                a1[M][j] = to_bf16(j < 4 ? weight_at(w.w1, true, (32u * M + col) * 4u + j) : 0.0f);
+        for (int M = 0; M < 2; ++M) a1[M] = T[kA1 + M * 64u + lane];
 #pragma unroll
         for (int Mo = 0; Mo < 2; ++Mo)
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
+            for (int s = 0; s < 4; ++s) a2[Mo][s] = T[kA2 + (Mo * 4u + s) * 64u + lane];
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    a2[Mo][s][j] = to_bf16(weight_at(w.w2, true, (32u * Mo + col) * 64u + k_unit(s, j, h)));
-        const uint32_t r = col % 4u;
-        const bool row_ok = col < 8u && (r < 2u || (r == 2u && w.wv != nullptr));
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                a3[s][j] = to_bf16(!row_ok ? 0.0f
-                                   : r == 2u ? weight_at(w.wv, true, k_unit(s, j, h))
-                                             : weight_at(w.w3, true, r * 64u + k_unit(s, j, h)));
+        for (int s = 0; s < 4; ++s) a3[s] = T[kA3 + s * 64u + lane];
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
         bv = w.bv ? w.bv[0] : 0.0f;
     }
-
-    static constexpr int kLds = 1;
-    __device__ static void fill_lds(const PolicyArgs&, float*) {}
 
     // Logit difference d = l1 - l0 and value v of this lane's environment; obs
     // is this lane's pre-step state.  The value row rides in the output tile at
@@ -227,7 +260,7 @@ struct MlpF32 {
         }
     }
 
-    __device__ void load(const PolicyArgs& w, uint32_t lane)
+    __device__ void load(const PolicyArgs& w, uint32_t lane, const float*)
     {
         const uint32_t col = lane % 32u;
 #pragma unroll
@@ -347,7 +380,7 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
     const DevParams& p = a.p;
 
     Mlp mlp;
-    mlp.load(w, lane);
+    mlp.load(w, lane, lds_w3);
 
     CartCore<REC, STATS> core(p, env);
     if (live) {
