@@ -92,8 +92,6 @@ __device__ __forceinline__ floatx16 bias_tile(const float* lds_b, uint32_t M, ui
 // ---------------------------------------------------------------------------
 struct MlpBf16 {
     bf16x8 a1[2];        // layer 1, row tiles 0/1; K = obs in k 0-3 and 8-11
-    bf16x8 a2[2][4];     // layer 2, [out tile][K step]
-    bf16x8 a3[4];        // layer 3, [K step]; rows 0,1 and 4,5 = the two logits, 2 and 6 = value
     float b3_0, b3_1, bv;
 
     // The lanes' operand vectors, staged once per workgroup in LDS as bfloat16
@@ -101,7 +99,8 @@ struct MlpBf16 {
     // in 4-7), A2 [Mo 2][s 4][64], A3 [s 4][64] (rows 0,1 / 4,5 the logits, 2 / 6
     // the value, per half).  The fill reads the weights in row-major order, so
     // global loads are coalesced, and scatters each to its permuted slot; each
-    // lane then reads 14 contiguous 16-byte vectors.
+    // lane then reads its 16-byte vectors: A1 once per launch into registers,
+    // A2 and A3 at every step (registers stay free for a third wave per SIMD).
     static constexpr uint32_t kA1 = 0, kA2 = 2 * 64, kA3 = kA2 + 8 * 64, kVecs = kA3 + 4 * 64;
     static constexpr int kLds = (int)kVecs * 4;   // floats: 16 B per vector
 
@@ -156,12 +155,6 @@ struct MlpBf16 {
         const bf16x8* T = reinterpret_cast<const bf16x8*>(lds);
 #pragma unroll
         for (int M = 0; M < 2; ++M) a1[M] = T[kA1 + M * 64u + lane];
-#pragma unroll
-        for (int Mo = 0; Mo < 2; ++Mo)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) a2[Mo][s] = T[kA2 + (Mo * 4u + s) * 64u + lane];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) a3[s] = T[kA3 + s * 64u + lane];
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
         bv = w.bv ? w.bv[0] : 0.0f;
@@ -171,9 +164,10 @@ struct MlpBf16 {
     // is this lane's pre-step state.  The value row rides in the output tile at
     // no extra cost, so VAL changes nothing here.
     template <bool VAL>
-    __device__ void eval(const CartState& obs, const float* lds_b1, const float* lds_b2, const float*, uint32_t lane,
-                         float& d, float& v) const
+    __device__ void eval(const CartState& obs, const float* lds_b1, const float* lds_b2, const float* lds,
+                         uint32_t lane, float& d, float& v) const
     {
+        const bf16x8* ops = reinterpret_cast<const bf16x8*>(lds);
         const uint32_t h = lane / 32u;
         const bf16x8 zero8 = {};
         bf16x8 own = zero8;
@@ -201,7 +195,7 @@ struct MlpBf16 {
             for (int Mo = 0; Mo < 2; ++Mo) {
                 c2[Mo] = bias_tile(lds_b2, Mo, h);
 #pragma unroll
-                for (int s = 0; s < 4; ++s) c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[Mo][s], b1[s], c2[Mo], 0, 0, 0);
+                for (int s = 0; s < 4; ++s) c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA2 + (Mo * 4u + s) * 64u + lane], b1[s], c2[Mo], 0, 0, 0);
             }
             bf16x8 b2[4];
 #pragma unroll
@@ -214,7 +208,7 @@ struct MlpBf16 {
             c3[1] = b3_1;
             c3[2] = bv;
 #pragma unroll
-            for (int s = 0; s < 4; ++s) c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[s], b2[s], c3, 0, 0, 0);
+            for (int s = 0; s < 4; ++s) c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA3 + s * 64u + lane], b2[s], c3, 0, 0, 0);
             if (h == T) {
                 l0 = c3[0];
                 l1 = c3[1];
