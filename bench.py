@@ -445,7 +445,7 @@ def policy_sweep(stream) -> dict:
                 for st in structs:
                     st.logp = st.value = None
             times = []
-            for r in range(3):
+            for r in range(5):
                 start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 start.record(stream)
                 for st in structs:
