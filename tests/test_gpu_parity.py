@@ -287,3 +287,16 @@ def test_max_envs_sampled():
     assert_bit_equal(g, merged)
     want = np.concatenate([ref[0]["stats"][0], ref[1]["stats"][0], ref[2]["stats"][0]])
     assert np.array_equal(g_stats, want)
+
+
+@pytest.mark.parametrize("D", [0, 5, 20])
+def test_env_results_independent_of_n(D):
+    """Environment e's trajectory, statistics row and final state do not depend on
+    how many environments the handle holds (kernel mapping, tiles, tails)."""
+    T, sched = 120, [50, 70]
+    small = gpu_run(300, T, sched, D=D, seed=12)
+    big = gpu_run(2000, T, sched, D=D, seed=12, slices=[(0, 300)])
+    assert_bit_equal(small, big)
+    # the first statistics row covers envs 0..255 in both runs
+    for a, b in zip(small["stats"], big["stats"]):
+        assert np.array_equal(a[0], b[0])

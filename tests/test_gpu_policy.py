@@ -253,6 +253,18 @@ def test_learner_batch_is_zero_copy_and_consistent():
     del keep
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_env_results_independent_of_n(dtype):
+    """The MLP mixes 64 environments per wave in its matrix tiles, but each
+    environment's outputs are its own column: the first 300 environments of a
+    1,000-env run equal a 300-env run bit for bit (p0, log pi, value, actions)."""
+    w = _weights(4, 0.3)
+    small = _gpu_policy_run(300, 32, 16, w, dtype, 6)
+    big = _gpu_policy_run(1000, 32, 16, w, dtype, 6, slices=[(0, 300)])
+    for k in ("obs", "action", "done", "p0", "logp", "value"):
+        assert np.array_equal(np.asarray(small[k]).view(np.uint8), np.asarray(big[k]).view(np.uint8)), k
+
+
 def test_policy_errors():
     import paper_2207_07736_amd as p
     w = workloads.mlp_weights(0)
