@@ -226,7 +226,7 @@ struct MlpBf16 {
 // independent accumulation chains that keep the matrix pipeline busy.
 // ---------------------------------------------------------------------------
 struct MlpF32 {
-    float a1[2][4];      // layer 1 [row tile][obs index]; both halves hold the same weight
+    float a1[2][2];      // layer 1 [row tile][K step]: W1[32 M + lane%32][2 s + lane/32]
     float b3_0, b3_1, bv;
 
     // LDS, filled once per workgroup:
@@ -256,11 +256,11 @@ struct MlpF32 {
 
     __device__ void load(const PolicyArgs& w, uint32_t lane, const float*)
     {
-        const uint32_t col = lane % 32u;
+        const uint32_t h = lane / 32u, col = lane % 32u;
 #pragma unroll
         for (int M = 0; M < 2; ++M)
 #pragma unroll
-            for (int s = 0; s < 4; ++s) a1[M][s] = weight_at(w.w1, false, (32u * M + col) * 4u + s);
+            for (int s = 0; s < 2; ++s) a1[M][s] = weight_at(w.w1, false, (32u * M + col) * 4u + 2u * s + h);
         b3_0 = w.b3 ? w.b3[0] : 0.0f;
         b3_1 = w.b3 ? w.b3[1] : 0.0f;
         bv = w.bv ? w.bv[0] : 0.0f;
@@ -272,17 +272,21 @@ struct MlpF32 {
                          uint32_t lane, float& d, float& v) const
     {
         const uint32_t h = lane / 32u;
-        const float own[4] = {obs.x, obs.xd, obs.th, obs.thd};
-        // layer 1, both tiles: K step s takes obs[s] from the tile's own half (k = T), 0 from the other
+        // layer 1, both tiles, two K steps of 2: K slot k of step s is obs component
+        // 2 s + k of the tile's environment, supplied by the lanes of half k.  A lane
+        // of half h holds its own environment (tile h); for the other tile it supplies
+        // the environment of lane ^ 32, exchanged once per step.
+        const float own0 = h ? obs.xd : obs.x, own1 = h ? obs.thd : obs.th;    // components h, 2 + h
+        const float give0 = h ? obs.x : obs.xd, give1 = h ? obs.th : obs.thd;  // the partner's h
+        const float other0 = __shfl_xor(give0, 32, 64), other1 = __shfl_xor(give1, 32, 64);
         floatx16 c1[2][2];
 #pragma unroll
         for (uint32_t T = 0; T < 2u; ++T)
 #pragma unroll
             for (int M = 0; M < 2; ++M) {
                 c1[T][M] = bias_tile(lds_b1, M, h);
-#pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    c1[T][M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][s], h == T ? own[s] : 0.0f, c1[T][M], 0, 0, 0);
+                c1[T][M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][0], h == T ? own0 : other0, c1[T][M], 0, 0, 0);
+                c1[T][M] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[M][1], h == T ? own1 : other1, c1[T][M], 0, 0, 0);
             }
 #pragma unroll
         for (int T = 0; T < 2; ++T)
