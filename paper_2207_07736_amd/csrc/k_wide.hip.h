@@ -66,6 +66,9 @@ struct BitRecorder {
 #define RL_REP16(X) RL_REP8(X) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15)
 #define RL_REP32(X) \
     RL_REP16(X) X(16) X(17) X(18) X(19) X(20) X(21) X(22) X(23) X(24) X(25) X(26) X(27) X(28) X(29) X(30) X(31)
+#define RL_REP64(X)                                                                                      \
+    RL_REP32(X) X(32) X(33) X(34) X(35) X(36) X(37) X(38) X(39) X(40) X(41) X(42) X(43) X(44) X(45) X(46) \
+        X(47) X(48) X(49) X(50) X(51) X(52) X(53) X(54) X(55) X(56) X(57) X(58) X(59) X(60) X(61) X(62) X(63)
 #define RL_FMA(i) "v_fma_f32 %[s" #i "], %[a" #i "], %[s" #i "], %[b" #i "]\n"
 #define RL_MUL(i) "v_mul_f32 %[s" #i "], %[a" #i "], %[s" #i "]\n"
 #define RL_ZERO(i) "v_mov_b32 %[s" #i "], 0\n"
@@ -100,21 +103,22 @@ __device__ __forceinline__ void replay_uniform_group(float (&s)[W], const float 
 {
     static_assert(O + N <= W, "group outside the lane's words");
     uint32_t cnt;
-    if constexpr (N == 32) RL_REPLAY_ASM(RL_REP32);
+    if constexpr (N == 64) RL_REPLAY_ASM(RL_REP64);
+    else if constexpr (N == 32) RL_REPLAY_ASM(RL_REP32);
     else if constexpr (N == 16) RL_REPLAY_ASM(RL_REP16);
     else if constexpr (N == 8) RL_REPLAY_ASM(RL_REP8);
     else RL_REPLAY_ASM(RL_REP4);
 }
 
 // All W words of the lane, in groups of at most kReplayGroup.
-constexpr int kReplayGroup = 32;
+constexpr int kReplayGroup = 64;
 template <int W, int O = 0>
 __device__ __forceinline__ void replay_uniform(float (&s)[W], const float (&pa)[W], const float (&pb)[W],
                                                uint32_t ub, uint32_t db, uint32_t m)
 {
     if constexpr (O < W) {
         constexpr int R = W - O;
-        constexpr int N = R >= kReplayGroup ? kReplayGroup : R >= 16 ? 16 : R >= 8 ? 8 : 4;
+        constexpr int N = R >= kReplayGroup ? kReplayGroup : R >= 32 ? 32 : R >= 16 ? 16 : R >= 8 ? 8 : 4;
         replay_uniform_group<N, O, W>(s, pa, pb, ub, db, m);
         replay_uniform<W, O + N>(s, pa, pb, ub, db, m);
     }
