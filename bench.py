@@ -415,6 +415,46 @@ def wide_only(D: int, steps: int, warmup: int) -> int:
     return 0
 
 
+def unfused_only(steps: int, warmup: int, copy_calibration: bool) -> int:
+    """Timed runs of the headline workload in its unfused form alone (for
+    profiling): 4,194,304 envs x 200 steps as 200 launches of K = 1, the state
+    read from and written to HBM at every step."""
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C3"]
+    n, T = w["n"], w["T"]
+    stream = torch.cuda.current_stream()
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    rows = [traj.rows(k, 1) for k in range(T)]
+    for _ in range(warmup):
+        for st in rows:
+            sim.step(1, st)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        for st in rows:
+            sim.step(1, st)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    algo = n * T * (workloads.TRAJ_BYTES_PER_ENV_STEP + 40) + T * (n // 256) * 16
+    print(json.dumps({"workload": w["name"] + " as 200 launches of K = 1", "ms_per_run": ms, "launch_ms": ms / T,
+                      "env_steps_per_s": n * T / (ms * 1e-3), "algorithmic_bytes_per_launch": algo // T,
+                      "algorithmic_GBs": algo / (ms * 1e-3) / 1e9}), flush=True)
+    del traj
+    sim.close()
+    if copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    return 0
+
+
 def policy_sweep(stream) -> dict:
     """The MLP-policy workload: 1,048,576 envs x 256 steps, fused K = 16 against
     unfused K = 1, fp32 and bf16 weights ~ N(0, 1/fan_in), zero biases; and K =
@@ -482,6 +522,8 @@ def main() -> int:
                     help="also run one plain device copy of 1 GiB (HBM counter calibration)")
     ap.add_argument("--policy", choices=("f32", "bf16"),
                     help="time only the MLP-policy workload (K = 16 launches) in this precision")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time only the headline workload as 200 launches of K = 1 (profiling)")
     ap.add_argument("--wide", type=int, metavar="D",
                     help="time only the state-size workload (262,144 envs, K = 500) with D padding words")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -492,6 +534,8 @@ def main() -> int:
         return policy_only(args.policy, args.steps, args.warmup)
     if args.wide:
         return wide_only(args.wide, args.steps, args.warmup)
+    if args.unfused:
+        return unfused_only(args.steps, args.warmup, args.copy_calibration)
 
     if args.ingest_pmc:
         w = workloads.WORKLOADS["C3"]
