@@ -15,8 +15,8 @@
 // register i holds row 8(i/4) + 4(l/32) + (i%4) of column l%32) each lane
 // already holds the values the next layer's B operand needs from it, provided
 // the next layer's K index runs over hidden units in that order; the weights are
-// gathered in that permuted order once per launch, so activations never move
-// between lanes.  The output layer puts logit rows at 0,1 (tile 0) and 4,5
+// placed in that permuted order once per workgroup (in LDS, or in registers for
+// the small tables), so activations never move between lanes.  The output layer puts logit rows at 0,1 (tile 0) and 4,5
 // (tile 1) so that every lane finds its own environment's logits in its own
 // registers 0 and 1, and the value row at 2 (tile 0) and 6 (tile 1), register 2.
 #pragma once
@@ -100,7 +100,8 @@ struct MlpBf16 {
     // the value, per half).  The fill reads the weights in row-major order, so
     // global loads are coalesced, and scatters each to its permuted slot; each
     // lane then reads its 16-byte vectors: A1 once per launch into registers,
-    // A2 and A3 at every step (registers stay free for a third wave per SIMD).
+    // A2 and A3 at every step (1 % faster than holding those 48 VGPRs; the kernel
+    // stays at two waves per SIMD either way).
     static constexpr uint32_t kA1 = 0, kA2 = 2 * 64, kA3 = kA2 + 8 * 64, kVecs = kA3 + 4 * 64;
     static constexpr int kLds = (int)kVecs * 4;   // floats: 16 B per vector
 
@@ -195,7 +196,9 @@ struct MlpBf16 {
             for (int Mo = 0; Mo < 2; ++Mo) {
                 c2[Mo] = bias_tile(lds_b2, Mo, h);
 #pragma unroll
-                for (int s = 0; s < 4; ++s) c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA2 + (Mo * 4u + s) * 64u + lane], b1[s], c2[Mo], 0, 0, 0);
+                for (int s = 0; s < 4; ++s)
+                    c2[Mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA2 + (Mo * 4u + s) * 64u + lane], b1[s],
+                                                                     c2[Mo], 0, 0, 0);
             }
             bf16x8 b2[4];
 #pragma unroll
@@ -208,7 +211,8 @@ struct MlpBf16 {
             c3[1] = b3_1;
             c3[2] = bv;
 #pragma unroll
-            for (int s = 0; s < 4; ++s) c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA3 + s * 64u + lane], b2[s], c3, 0, 0, 0);
+            for (int s = 0; s < 4; ++s)
+                c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ops[kA3 + s * 64u + lane], b2[s], c3, 0, 0, 0);
             if (h == T) {
                 l0 = c3[0];
                 l1 = c3[1];
