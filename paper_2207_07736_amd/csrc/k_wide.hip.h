@@ -124,9 +124,10 @@ __device__ __forceinline__ void replay_uniform(float (&s)[W], const float (&pa)[
     }
 }
 
-// Phase 2: G lanes per environment, W consecutive words per lane (W a multiple
-// of 4, loaded as float4).  Replays `steps` steps from the LDS bits for the
-// 64 / G environments a wave covers at a time, for all of the wave's 64 envs.
+// Phase 2: G lanes per environment, W words per lane (W a multiple of 4, held
+// as W / 4 float4 runs interleaved across the group's lanes).  Replays `steps`
+// steps from the LDS bits for the 64 / G environments a wave covers at a time,
+// for all of the wave's 64 envs.
 template <int G, int W>
 __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t* lds_u, const uint32_t* lds_d,
                                                uint32_t steps, uint32_t blk)
