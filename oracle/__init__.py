@@ -128,6 +128,11 @@ def lib():
     L.orc_set_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
     L.orc_set_state.restype = ctypes.c_int
     L.orc_get_pad_params.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    L.orc_check_rows.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
+                                 ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32)]
+    L.orc_check_rows.restype = ctypes.c_uint64
     L.orc_get_pad_params.restype = None
     _lib = L
     return L
@@ -342,3 +347,21 @@ class Sim:
         b = np.empty((self.D, self.n), dtype=np.float32)
         lib().orc_get_pad_params(self._h, a.ctypes.data, b.ctypes.data)
         return a, b
+
+
+def check_rows(params: Params, seed: int, env0: int, t0: int, obs, action, reward, done, ep0=None):
+    """Teacher-forced check of recorded random-action rows ([K][4][n] obs,
+    [K][n] action / reward / done for envs env0 ..): returns (number of
+    mismatching env-steps, (k, i) of the first or None)."""
+    obs = np.ascontiguousarray(obs, dtype=np.float32)
+    action = np.ascontiguousarray(action, dtype=np.uint8)
+    reward = np.ascontiguousarray(reward, dtype=np.float32)
+    done = np.ascontiguousarray(done, dtype=np.uint8)
+    K, four, n = obs.shape
+    assert four == 4 and action.shape == reward.shape == done.shape == (K, n)
+    e = None if ep0 is None else np.ascontiguousarray(ep0, dtype=np.uint32)
+    bk, bi = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    bad = lib().orc_check_rows(ctypes.byref(params), int(seed), int(env0), int(n), int(t0), int(K),
+                               None if e is None else e.ctypes.data, obs.ctypes.data, action.ctypes.data,
+                               reward.ctypes.data, done.ctypes.data, ctypes.byref(bk), ctypes.byref(bi))
+    return int(bad), ((int(bk.value), int(bi.value)) if bad else None)

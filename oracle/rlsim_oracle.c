@@ -526,3 +526,61 @@ void orc_get_pad_params(const orc_sim* sim, float* a, float* b)
     if (a && nd) memcpy(a, sim->a, nd * sizeof(float));
     if (b && nd) memcpy(b, sim->b, nd * sizeof(float));
 }
+
+/* ------------------------------------------------------------------------ */
+/* Teacher-forced check of recorded random-action rows (a test helper: the    */
+/* comparison rule that every recorded step follows from the one before it).  */
+/* Rows k = 0..K-1 hold global steps t0 + k of environments env0 .. env0+n-1, */
+/* laid out [K][4][n] (obs) and [K][n] (action, reward, done); ep0[i] is the   */
+/* episode's step count at t0 (NULL: 0 for every env, as after a reset).  For */
+/* every env-step it recomputes, from the recorded obs and nothing else:      */
+/*   the random action bit of (seed, env, t), reward 1,                       */
+/*   next = the simulation step of (obs_t, action),                           */
+/*   done = terminated(next) | truncated << 1 (episode length from ep0),      */
+/*   obs_{t+1} (row k+1) = the reset draw for step t+1 if done, else next,    */
+/* bit for bit.  Returns the number of mismatching env-steps and, if any, the */
+/* row and env index of the first in *bad_k, *bad_i.                         */
+/* ------------------------------------------------------------------------ */
+uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint32_t n, uint32_t t0, uint32_t K,
+                        const uint32_t* ep0, const float* obs, const uint8_t* act, const float* rew,
+                        const uint8_t* done, uint32_t* bad_k, uint32_t* bad_i)
+{
+    uint64_t bad = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        uint32_t ep = ep0 ? ep0[i] : 0u;
+        uint32_t env = env0 + i;
+        for (uint32_t k = 0; k < K; ++k) {
+            uint32_t t = t0 + k;
+            float cur[4], nxt[4];
+            for (int c = 0; c < 4; ++c) cur[c] = obs[((size_t)k * 4 + c) * n + i];
+            int a = orc_action_bit(seed, env, t);
+            orc_env_step(p, cur, a, nxt);
+            uint32_t len = ep + 1u;
+            int term = orc_terminated(p, nxt);
+            int trunc = (p->max_episode_steps != 0u) && (len >= p->max_episode_steps);
+            uint8_t d = (uint8_t)(term | (trunc << 1));
+            int ok = act[(size_t)k * n + i] == (uint8_t)a && rew[(size_t)k * n + i] == 1.0f &&
+                     done[(size_t)k * n + i] == d;
+            if (d) {
+                orc_reset_draw(p, seed, env, t + 1u, nxt);
+                ep = 0u;
+            } else {
+                ep = len;
+            }
+            if (ok && k + 1 < K) {
+                for (int c = 0; c < 4; ++c) {
+                    float g = obs[((size_t)(k + 1) * 4 + c) * n + i];
+                    if (memcmp(&g, &nxt[c], sizeof(float)) != 0) ok = 0;
+                }
+            }
+            if (!ok) {
+                if (bad == 0 && bad_k && bad_i) {
+                    *bad_k = k;
+                    *bad_i = i;
+                }
+                ++bad;
+            }
+        }
+    }
+    return bad;
+}

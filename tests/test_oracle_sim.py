@@ -266,3 +266,35 @@ def test_episodes_last_at_least_eight_steps():
     for _ in range(7):
         s = oracle.cartpole_step(P, s, 0)
     assert oracle.terminated(P, oracle.cartpole_step(P, s, 0))
+
+
+@pytest.mark.parametrize("over", [{}, {"max_episode_steps": 7}, {"x_threshold": 0.3}, {"compute_factor": 3}])
+def test_row_checker_accepts_oracle_rows_and_finds_planted_errors(over):
+    """orc_check_rows (the teacher-forced check GPU tests run at full size) passes
+    the oracle's own trajectory and flags a corrupted obs, action, reward or done
+    at the row and env where it was planted."""
+    params = oracle.make_params(**workloads.cartpole(**over))
+    n, T, env0, seed = 97, 60, 1000, 5
+    sim = oracle.Sim(n, 0, params, env0=env0)
+    sim.reset(seed)
+    tr = sim.step(T)
+    assert oracle.check_rows(params, seed, env0, 0, tr["obs"], tr["action"], tr["reward"], tr["done"]) == (0, None)
+    for field, k, i in (("obs", 17, 40), ("action", 3, 96), ("reward", 59, 0), ("done", 30, 13)):
+        bad = {key: tr[key].copy() for key in ("obs", "action", "reward", "done")}
+        if field == "obs":
+            bad["obs"][k, 2, i] = np.nextafter(bad["obs"][k, 2, i], np.float32(1))
+        elif field == "action":
+            bad["action"][k, i] ^= 1
+        elif field == "reward":
+            bad["reward"][k, i] = 0.5
+        else:
+            bad["done"][k, i] ^= 2
+        count, first = oracle.check_rows(params, seed, env0, 0, bad["obs"], bad["action"], bad["reward"], bad["done"])
+        # an obs error shows at the step that produced it (row k - 1 predicts row k)
+        want_k = k - 1 if field == "obs" else k
+        assert count >= 1 and first == (want_k, i), (field, count, first)
+    # a later start: rows from step t0 with the episode counters at t0
+    st, ep, t = sim.get_state()
+    tr2 = sim.step(25)
+    assert oracle.check_rows(params, seed, env0, t, tr2["obs"], tr2["action"], tr2["reward"], tr2["done"],
+                             ep0=ep) == (0, None)
