@@ -1,6 +1,7 @@
 /*
- * rlsim_probe.h -- C ABI of the store-only probe of the trajectory layout
- * (librlsim_probe.so), a measurement aid beside librlsim.so.
+ * rlsim_probe.h -- C ABI of the measurement aids beside librlsim.so
+ * (librlsim_probe.so): the store-only probe of the trajectory layout, and the
+ * error probe of the policy kernel's elementwise functions.
  *
  * The fused simulator kernel's unavoidable work is writing the trajectory
  * (section "Simulator Kernel Fusion": fusion removes the state round trips,
@@ -35,6 +36,25 @@ extern "C" {
  * (RLSIM_EDEVICE) if the launch fails. */
 int rlsim_probe_store(uint32_t n, uint32_t K, float* obs, uint8_t* action, float* reward, uint8_t* done,
                       void* stream);
+
+/* Error of the MLP-policy kernel's elementwise functions, measured at every
+ * fp32 value x whose bit pattern lies in [lo_bits, lo_bits + count) (NaN and
+ * infinities skipped), against double-precision evaluations of what they
+ * compute (the policy of rlsim.h: tanh hidden units, softmax over two logits,
+ * log pi of the action taken):
+ *   out_max[0] = max |tanh_kernel(x) - tanh(x)|
+ *   out_max[1] = max |p0_kernel(x) - 1 / (1 + e^x)|          (x = l1 - l0)
+ *   out_max[2] = max over a in {0, 1} of |log_pi_kernel(x, a) - r| / (1 + |r|),
+ *                r = -softplus(a ? -x : x)
+ * each as the bit pattern of a non-negative float rounded up, merged with
+ * atomic max into the caller-owned DEVICE array out_max[3] (zero it first;
+ * several calls over parts of a range merge).  The functions are those the
+ * policy kernel itself calls, so the maxima over all 2^32 patterns bound the
+ * kernel's elementwise error; the oracle's tolerance for the policy outputs is
+ * built on them.
+ * Errors: -1 if count == 0, lo_bits + count > 2^32, or out_max is NULL or not
+ * 4-byte aligned; -3 if the launch fails. */
+int rlsim_probe_policy_math(uint32_t lo_bits, uint64_t count, uint32_t* out_max, void* stream);
 
 #ifdef __cplusplus
 }

@@ -59,6 +59,19 @@ class Params(ctypes.Structure):
     ]
 
 
+class Errs(ctypes.Structure):
+    """Error model of a device policy evaluation (orc_mlp_bounds): per-operation
+    accumulation bound, and absolute errors of tanh, p0 and (relative to
+    1 + |log pi|) log pi."""
+    _fields_ = [("acc", ctypes.c_double), ("tanh", ctypes.c_double), ("p0", ctypes.c_double),
+                ("logpi", ctypes.c_double)]
+
+
+class Bounds(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_double) for name in ("p0_lo", "p0_hi", "lp0_lo", "lp0_hi", "lp1_lo", "lp1_hi",
+                                                     "v_lo", "v_hi")]
+
+
 class _Policy(ctypes.Structure):
     _fields_ = [("bf16", ctypes.c_int)] + [
         (name, ctypes.POINTER(ctypes.c_float)) for name in ("w1", "b1", "w2", "b2", "w3", "b3", "wv", "bv")
@@ -133,6 +146,17 @@ def lib():
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32)]
     L.orc_check_rows.restype = ctypes.c_uint64
+    L.orc_mlp_bounds.argtypes = [ctypes.POINTER(_Policy), ctypes.POINTER(ctypes.c_float), ctypes.POINTER(Errs),
+                                 ctypes.POINTER(Bounds)]
+    L.orc_mlp_bounds.restype = None
+    L.orc_check_policy_rows.argtypes = [ctypes.POINTER(Params), ctypes.POINTER(_Policy), ctypes.c_uint64,
+                                        ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.POINTER(Errs), ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint32),
+                                        ctypes.POINTER(ctypes.c_uint32)]
+    L.orc_check_policy_rows.restype = ctypes.c_uint64
     L.orc_get_pad_params.restype = None
     _lib = L
     return L
@@ -271,6 +295,16 @@ class Policy:
         logit, _, _ = self.eval(obs)
         return log_prob(logit, action)
 
+    def bounds(self, obs, errs: "Errs") -> dict:
+        """Enclosures (lo, hi) of p0, log pi(0), log pi(1) and the value that a
+        device evaluation under the error model errs may return for obs."""
+        o = np.ascontiguousarray(obs, dtype=np.float32)
+        b = Bounds()
+        lib().orc_mlp_bounds(ctypes.byref(self.struct), o.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                             ctypes.byref(errs), ctypes.byref(b))
+        return dict(p0=(b.p0_lo, b.p0_hi), logp0=(b.lp0_lo, b.lp0_hi), logp1=(b.lp1_lo, b.lp1_hi),
+                    value=(b.v_lo, b.v_hi))
+
 
 def log_prob(logit, action: int) -> float:
     """log softmax(logit)[action] for two logits."""
@@ -365,3 +399,27 @@ def check_rows(params: Params, seed: int, env0: int, t0: int, obs, action, rewar
                                None if e is None else e.ctypes.data, obs.ctypes.data, action.ctypes.data,
                                reward.ctypes.data, done.ctypes.data, ctypes.byref(bk), ctypes.byref(bi))
     return int(bad), ((int(bk.value), int(bi.value)) if bad else None)
+
+
+def check_policy_rows(params: Params, policy: "Policy", seed: int, env0: int, t0: int, obs, action, reward, done,
+                      p0, errs: "Errs", logp=None, value=None, ep0=None):
+    """Teacher-forced check of recorded policy rows against the enclosures of
+    orc_mlp_bounds under errs.  Returns (failing env-steps, first failure (k, i)
+    or None, stats) with stats = dict(worst: max |p0 - oracle p0|, max_width and
+    mean_width of the p0 enclosures, exempt: actions that differ from the
+    oracle's own choice, necessarily with u inside the enclosure)."""
+    c = lambda x, dt: None if x is None else np.ascontiguousarray(x, dtype=dt)  # noqa: E731
+    obs, action, reward, done = c(obs, np.float32), c(action, np.uint8), c(reward, np.float32), c(done, np.uint8)
+    p0, logp, value, ep0 = c(p0, np.float32), c(logp, np.float32), c(value, np.float32), c(ep0, np.uint32)
+    K, four, n = obs.shape
+    assert four == 4 and action.shape == reward.shape == done.shape == p0.shape == (K, n)
+    ptr = lambda x: None if x is None else x.ctypes.data  # noqa: E731
+    st = (ctypes.c_double * 3)()
+    ex = ctypes.c_uint64(0)
+    bk, bi = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    bad = lib().orc_check_policy_rows(ctypes.byref(params), ctypes.byref(policy.struct), int(seed), int(env0), int(n),
+                                      int(t0), int(K), ptr(ep0), ptr(obs), ptr(action), ptr(reward), ptr(done),
+                                      ptr(p0), ptr(logp), ptr(value), ctypes.byref(errs), st, ctypes.byref(ex),
+                                      ctypes.byref(bk), ctypes.byref(bi))
+    stats = dict(worst=st[0], max_width=st[1], mean_width=st[2] / max(1, K * n), exempt=int(ex.value))
+    return int(bad), ((int(bk.value), int(bi.value)) if bad else None), stats

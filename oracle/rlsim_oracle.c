@@ -23,6 +23,10 @@
  * (known-answer Philox words, hand-derived rational cart-pole steps, a
  * 50-digit Euler-Lagrange solve, linearisation, conservation laws, closed
  * forms of the padding recurrence and of special MLP weights).
+ *
+ * At the end of the file are test helpers built on these definitions: the
+ * teacher-forced row checkers, and orc_mlp_bounds, the interval enclosure of
+ * a device evaluation of the policy that serves as its tolerance.
  */
 #include <math.h>
 #include <stdint.h>
@@ -248,10 +252,12 @@ float orc_pad_update(float s, float a, float b, int u)
 /* the usual actor-critic form of the learner the collected data feeds).     */
 /* bf16 mode rounds the weights, the input and both hidden activations to    */
 /* bfloat16 (round to nearest even) at the points where a bf16 kernel holds  */
-/* them; biases and sums stay in double.                                     */
+/* them; biases and sums stay in double.  bf16 = 2 is bf16 mode over weight */
+/* arrays that already hold bf16 values (rounding them again would change   */
+/* nothing), so only the input and the activations are rounded.              */
 /* ------------------------------------------------------------------------ */
 typedef struct {
-    int bf16;
+    int bf16;                                   /* 0 fp32, 1 bf16, 2 bf16 with rounded weights */
     const float *w1, *b1, *w2, *b2, *w3, *b3;   /* biases may be NULL (zero) */
     const float *wv, *bv;                       /* value head 1 x 64, 1; wv NULL = none */
 } orc_policy;
@@ -280,7 +286,7 @@ double orc_round_bf16(double v)
 static double orc_w(const orc_policy* pol, const float* w, int idx)
 {
     double v = (double)w[idx];
-    return pol->bf16 ? orc_round_bf16(v) : v;
+    return pol->bf16 == 1 ? orc_round_bf16(v) : v;
 }
 
 /* The trunk: h2 = tanh(W2 tanh(W1 obs + b1) + b2). */
@@ -337,6 +343,126 @@ double orc_log_prob(const double logit[2], int a)
     double m = logit[0] > logit[1] ? logit[0] : logit[1];
     double lse = m + log(exp(logit[0] - m) + exp(logit[1] - m));
     return logit[a ? 1 : 0] - lse;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Tolerance of a device evaluation of the policy (a test helper): interval  */
+/* enclosures of what any evaluation under the following error model may     */
+/* return for one observation.                                               */
+/*  - Each dot product bias + sum of n products is formed in fp32 with an    */
+/*    error of at most err->acc * (n + 1) * (|bias| + sum |w x|), over the    */
+/*    operands actually used (acc = 2^-23, twice fp32's unit roundoff per    */
+/*    operation, covers any summation order and rounding direction; products */
+/*    of bf16 values are exact in fp32, fp32 products round once).           */
+/*  - tanh and p0 = 1 / (1 + e^d) are returned with an absolute error of at  */
+/*    most err->tanh and err->p0, log pi with at most                         */
+/*    err->logpi * (1 + |log pi|); d = l1 - l0 is one more fp32 rounding.     */
+/*  - In bf16 mode inputs, weights and activations are rounded to bf16 at the */
+/*    points the oracle rounds them.  Rounding is monotone, so rounding the   */
+/*    ends of an interval encloses the rounding of every point inside it.    */
+/* Intervals are carried as centre and radius through the dot products and   */
+/* as end points through the monotone functions.  Out: lo/hi of p0, of        */
+/* log pi(0), of log pi(1), and of the value head (0 without one).           */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    double acc, tanh, p0, logpi;
+} orc_errs;
+
+typedef struct {
+    double p0_lo, p0_hi, lp0_lo, lp0_hi, lp1_lo, lp1_hi, v_lo, v_hi;
+} orc_bounds;
+
+static double orc_dmax(double a, double b) { return a > b ? a : b; }
+
+/* An activation interval from a pre-activation interval [z - r, z + r]. */
+static void orc_act_interval(const orc_policy* pol, const orc_errs* e, double z, double r, double* lo, double* hi)
+{
+    double a = tanh(z - r) - e->tanh;
+    double b = tanh(z + r) + e->tanh;
+    if (pol->bf16) {
+        a = orc_round_bf16(a);
+        b = orc_round_bf16(b);
+    }
+    *lo = a;
+    *hi = b;
+}
+
+/* -softplus(z), the log-probability of the action whose logit is z below the other's */
+static double orc_neg_softplus(double z)
+{
+    return -(orc_dmax(z, 0.0) + log1p(exp(-fabs(z))));
+}
+
+void orc_mlp_bounds(const orc_policy* pol, const float obs[4], const orc_errs* e, orc_bounds* out)
+{
+    double x[4], lo1[64], hi1[64], lo2[64], hi2[64];
+    for (int i = 0; i < 4; ++i) x[i] = pol->bf16 ? orc_round_bf16((double)obs[i]) : (double)obs[i];
+    /* layer 1: exact inputs */
+    for (int o = 0; o < 64; ++o) {
+        double b = pol->b1 ? (double)pol->b1[o] : 0.0;
+        double z = b, mag = fabs(b);
+        for (int i = 0; i < 4; ++i) {
+            double t = orc_w(pol, pol->w1, o * 4 + i) * x[i];
+            z += t;
+            mag += fabs(t);
+        }
+        orc_act_interval(pol, e, z, e->acc * 5.0 * mag, &lo1[o], &hi1[o]);
+    }
+    /* layer 2: interval inputs */
+    for (int o = 0; o < 64; ++o) {
+        double b = pol->b2 ? (double)pol->b2[o] : 0.0;
+        double z = b, rad = 0.0, mag = fabs(b);
+        for (int i = 0; i < 64; ++i) {
+            double w = orc_w(pol, pol->w2, o * 64 + i);
+            z += w * 0.5 * (lo1[i] + hi1[i]);
+            rad += fabs(w) * 0.5 * (hi1[i] - lo1[i]);
+            mag += fabs(w) * orc_dmax(fabs(lo1[i]), fabs(hi1[i]));
+        }
+        orc_act_interval(pol, e, z, rad + e->acc * 65.0 * mag, &lo2[o], &hi2[o]);
+    }
+    /* logits: d = l1 - l0 carried directly (l0 and l1 share h2) */
+    double d = 0.0, rad_d = 0.0, mag0 = 0.0, mag1 = 0.0;
+    {
+        double b0 = pol->b3 ? (double)pol->b3[0] : 0.0, b1 = pol->b3 ? (double)pol->b3[1] : 0.0;
+        d = b1 - b0;
+        mag0 = fabs(b0);
+        mag1 = fabs(b1);
+        for (int i = 0; i < 64; ++i) {
+            double w0 = orc_w(pol, pol->w3, i), w1 = orc_w(pol, pol->w3, 64 + i);
+            double m = orc_dmax(fabs(lo2[i]), fabs(hi2[i]));
+            d += (w1 - w0) * 0.5 * (lo2[i] + hi2[i]);
+            rad_d += fabs(w1 - w0) * 0.5 * (hi2[i] - lo2[i]);
+            mag0 += fabs(w0) * m;
+            mag1 += fabs(w1) * m;
+        }
+        rad_d += e->acc * 65.0 * (mag0 + mag1);
+        rad_d += 0.5 * e->acc * (fabs(d) + rad_d);      /* the subtraction l1 - l0 */
+    }
+    double dlo = d - rad_d, dhi = d + rad_d;
+    out->p0_lo = 1.0 / (1.0 + exp(dhi)) - e->p0;         /* p0 decreases with d */
+    out->p0_hi = 1.0 / (1.0 + exp(dlo)) + e->p0;
+    /* log pi(0) = -softplus(d) decreases with d; log pi(1) = -softplus(-d) increases */
+    double a0 = orc_neg_softplus(dhi), b0 = orc_neg_softplus(dlo);
+    double a1 = orc_neg_softplus(-dlo), b1 = orc_neg_softplus(-dhi);
+    out->lp0_lo = a0 - e->logpi * (1.0 + fabs(a0));
+    out->lp0_hi = b0 + e->logpi * (1.0 + fabs(b0));
+    out->lp1_lo = a1 - e->logpi * (1.0 + fabs(a1));
+    out->lp1_hi = b1 + e->logpi * (1.0 + fabs(b1));
+    if (pol->wv) {
+        double bv = pol->bv ? (double)pol->bv[0] : 0.0;
+        double v = bv, rad = 0.0, mag = fabs(bv);
+        for (int i = 0; i < 64; ++i) {
+            double w = orc_w(pol, pol->wv, i);
+            v += w * 0.5 * (lo2[i] + hi2[i]);
+            rad += fabs(w) * 0.5 * (hi2[i] - lo2[i]);
+            mag += fabs(w) * orc_dmax(fabs(lo2[i]), fabs(hi2[i]));
+        }
+        rad += e->acc * 65.0 * mag;
+        out->v_lo = v - rad;
+        out->v_hi = v + rad;
+    } else {
+        out->v_lo = out->v_hi = 0.0;
+    }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -582,5 +708,105 @@ uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint3
             }
         }
     }
+    return bad;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Teacher-forced check of recorded policy rows (a test helper).  As          */
+/* orc_check_rows, with the MLP policy choosing the action: for every         */
+/* env-step, with u the POLICY-stream uniform of (seed, env, t) and p0g the   */
+/* recorded probability of action 0:                                          */
+/*   the recorded action is (u < p0g ? 0 : 1)               (exact);          */
+/*   p0g, and log pi / value when given, lie in orc_mlp_bounds' enclosures    */
+/*   for the recorded obs (the recorded action's log pi);                    */
+/*   reward 1, the done byte, and the next row (reset draw after an episode   */
+/*   end) follow from the simulation step of (obs, recorded action), bit for  */
+/*   bit.                                                                    */
+/* An action that differs from the oracle's own choice (u < p0) can only be   */
+/* one whose u lies inside the p0 enclosure; these are counted in *exempt.    */
+/* stats (may be NULL): [0] max |p0g - p0|, [1] max p0 enclosure width,        */
+/* [2] sum of p0 enclosure widths.  Returns the number of failing env-steps;  */
+/* *bad_k, *bad_i the first failure.                                          */
+/* ------------------------------------------------------------------------ */
+uint64_t orc_check_policy_rows(const orc_params* p, const orc_policy* pol, uint64_t seed, uint32_t env0, uint32_t n,
+                               uint32_t t0, uint32_t K, const uint32_t* ep0, const float* obs, const uint8_t* act,
+                               const float* rew, const uint8_t* done, const float* p0g, const float* logp,
+                               const float* value, const orc_errs* errs, double stats[3], uint64_t* exempt,
+                               uint32_t* bad_k, uint32_t* bad_i)
+{
+    uint64_t bad = 0, ex = 0;
+    double worst = 0.0, wmax = 0.0, wsum = 0.0;
+    /* a bf16 policy is evaluated over weight copies rounded once up front */
+    float rw1[64 * 4], rw2[64 * 64], rw3[2 * 64], rwv[64];
+    orc_policy rp = *pol;
+    if (pol->bf16 == 1) {
+        for (int j = 0; j < 64 * 4; ++j) rw1[j] = (float)orc_round_bf16((double)pol->w1[j]);
+        for (int j = 0; j < 64 * 64; ++j) rw2[j] = (float)orc_round_bf16((double)pol->w2[j]);
+        for (int j = 0; j < 2 * 64; ++j) rw3[j] = (float)orc_round_bf16((double)pol->w3[j]);
+        for (int j = 0; j < 64 && pol->wv; ++j) rwv[j] = (float)orc_round_bf16((double)pol->wv[j]);
+        rp.w1 = rw1;
+        rp.w2 = rw2;
+        rp.w3 = rw3;
+        rp.wv = pol->wv ? rwv : NULL;
+        rp.bf16 = 2;
+    }
+    for (uint32_t i = 0; i < n; ++i) {
+        uint32_t ep = ep0 ? ep0[i] : 0u;
+        uint32_t env = env0 + i;
+        for (uint32_t k = 0; k < K; ++k) {
+            uint32_t t = t0 + k;
+            size_t q = (size_t)k * n + i;
+            float cur[4], nxt[4];
+            for (int c = 0; c < 4; ++c) cur[c] = obs[((size_t)k * 4 + c) * n + i];
+            int a = act[q];
+            float u = orc_policy_u(seed, env, t);
+            double logit[2], p0, v;
+            orc_bounds bd;
+            orc_mlp_eval(&rp, cur, logit, &p0, &v);
+            orc_mlp_bounds(&rp, cur, errs, &bd);
+            double g = (double)p0g[q];
+            if (fabs(g - p0) > worst) worst = fabs(g - p0);
+            if (bd.p0_hi - bd.p0_lo > wmax) wmax = bd.p0_hi - bd.p0_lo;
+            wsum += bd.p0_hi - bd.p0_lo;
+            int ok = (a == (u < p0g[q] ? 0 : 1)) && g >= bd.p0_lo && g <= bd.p0_hi;
+            if (a != (((double)u < p0) ? 0 : 1)) ++ex;
+            if (logp) {
+                double l = (double)logp[q];
+                if (a ? (l < bd.lp1_lo || l > bd.lp1_hi) : (l < bd.lp0_lo || l > bd.lp0_hi)) ok = 0;
+            }
+            if (value && ((double)value[q] < bd.v_lo || (double)value[q] > bd.v_hi)) ok = 0;
+            orc_env_step(p, cur, a, nxt);
+            uint32_t len = ep + 1u;
+            int term = orc_terminated(p, nxt);
+            int trunc = (p->max_episode_steps != 0u) && (len >= p->max_episode_steps);
+            uint8_t d = (uint8_t)(term | (trunc << 1));
+            if (rew[q] != 1.0f || done[q] != d) ok = 0;
+            if (d) {
+                orc_reset_draw(p, seed, env, t + 1u, nxt);
+                ep = 0u;
+            } else {
+                ep = len;
+            }
+            if (ok && k + 1 < K) {
+                for (int c = 0; c < 4; ++c) {
+                    float gnext = obs[((size_t)(k + 1) * 4 + c) * n + i];
+                    if (memcmp(&gnext, &nxt[c], sizeof(float)) != 0) ok = 0;
+                }
+            }
+            if (!ok) {
+                if (bad == 0 && bad_k && bad_i) {
+                    *bad_k = k;
+                    *bad_i = i;
+                }
+                ++bad;
+            }
+        }
+    }
+    if (stats) {
+        stats[0] = worst;
+        stats[1] = wmax;
+        stats[2] = wsum;
+    }
+    if (exempt) *exempt = ex;
     return bad;
 }

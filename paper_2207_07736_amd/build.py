@@ -1,5 +1,6 @@
 """Build librlsim.so (the HIP kernels and the C ABI) and librlsim_probe.so (the
-store-only probe the bench measures the store ceiling with) for gfx950 with hipcc.
+store-only probe the bench measures the store ceiling with, and the error probe
+of the policy kernel's elementwise functions) for gfx950 with hipcc.
 
 Floating-point flags matter for the results: no contraction of a*b+c into an
 FMA unless written, IEEE single-precision division, denormals kept, and no
@@ -15,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "rlsim.hip")
 LIB = os.path.join(HERE, "librlsim.so")
-PROBE_SRC = os.path.join(HERE, "csrc", "store_probe.hip")
+PROBE_SRCS = [os.path.join(HERE, "csrc", "store_probe.hip")]      # includes math_probe.hip.h
 PROBE_LIB = os.path.join(HERE, "librlsim_probe.so")
 INCLUDE = os.path.join(ROOT, "include")
 
@@ -43,16 +44,16 @@ def sources():
 
 
 def build(verbose: bool = False) -> str:
-    """Compile csrc/rlsim.hip into librlsim.so and csrc/store_probe.hip into
+    """Compile csrc/rlsim.hip into librlsim.so and the probe sources into
     librlsim_probe.so next to this file (always).  Returns the main library."""
-    _compile(SRC, LIB, verbose)
-    _compile(PROBE_SRC, PROBE_LIB, verbose)
+    _compile([SRC], LIB, verbose)
+    _compile(PROBE_SRCS, PROBE_LIB, verbose)
     return LIB
 
 
-def _compile(src: str, lib: str, verbose: bool) -> None:
+def _compile(srcs: list, lib: str, verbose: bool) -> None:
     tmp = lib + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-o", tmp, src]
+    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-o", tmp, *srcs]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -67,6 +67,12 @@ __device__ __forceinline__ float tanh_fast(float x)
     return __builtin_fmaf(-2.0f, __builtin_amdgcn_rcpf(1.0f + e), 1.0f);
 }
 
+// softmax over two logits, from d = l1 - l0: p0 = 1 / (1 + e^d)
+__device__ __forceinline__ float policy_p0(float d)
+{
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(d * 1.44269504088896340736f));
+}
+
 __device__ __forceinline__ float weight_at(const void* w, bool bf16, uint32_t idx)
 {
     if (bf16) {
@@ -405,8 +411,7 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
         const float u = u24(pick_word(pw, t & 3u));
         float d, v;
         mlp.template eval<OUT>(core.s, lds_b1, lds_b2, lds_w3, lane, d, v);
-        // softmax over two logits: p0 = 1 / (1 + e^(l1 - l0))
-        const float p0 = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(d * 1.44269504088896340736f));
+        const float p0 = policy_p0(d);
         const uint32_t act = (u < p0) ? 0u : 1u;
         if (live) {
             if (OUT) {

@@ -1,7 +1,9 @@
-// store_probe.hip -- the store-only probe of include/rlsim_probe.h: the fused
-// kernel's trajectory stores (same planes, same per-lane offsets laundered
-// through an empty asm, same scalar row bases, same workgroup mapping) with
-// the simulation taken out.
+// store_probe.hip -- the probe library of include/rlsim_probe.h.  Here the
+// store-only probe: the fused kernel's trajectory stores (same planes, same
+// per-lane offsets laundered through an empty asm, same scalar row bases, same
+// workgroup mapping) with the simulation taken out.  The policy-math error
+// probe is math_probe.hip.h, included at the end (one translation unit: the
+// kernel headers define kernels).
 #include <hip/hip_runtime.h>
 
 #include "rlsim_probe.h"
@@ -49,3 +51,5 @@ extern "C" int rlsim_probe_store(uint32_t n, uint32_t K, float* obs, uint8_t* ac
     hipLaunchKernelGGL(rlsim_dev::k_store_probe, grid, block, 0, (hipStream_t)stream, n, K, obs, action, reward, done);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
+
+#include "math_probe.hip.h"

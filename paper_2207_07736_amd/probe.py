@@ -1,5 +1,6 @@
 """Thin ctypes binding of librlsim_probe.so (include/rlsim_probe.h): the
-store-only probe of the trajectory layout, a measurement aid.  Argument
+store-only probe of the trajectory layout and the error probe of the policy
+kernel's elementwise functions, measurement aids.  Argument
 marshalling only; fails loudly if the library has not been built."""
 from __future__ import annotations
 
@@ -8,7 +9,7 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
-PROBE_EXPORTS = ("rlsim_probe_store",)
+PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math")
 
 
 def _load():
@@ -18,6 +19,8 @@ def _load():
     u32, vp = ctypes.c_uint32, ctypes.c_void_p
     L.rlsim_probe_store.argtypes = [u32, u32, vp, vp, vp, vp, vp]
     L.rlsim_probe_store.restype = ctypes.c_int
+    L.rlsim_probe_policy_math.argtypes = [u32, ctypes.c_uint64, vp, vp]
+    L.rlsim_probe_policy_math.restype = ctypes.c_int
     return L
 
 
@@ -35,3 +38,13 @@ def probe_store(n: int, K: int, obs, action, reward, done, stream=None) -> None:
     rc = probe_lib.rlsim_probe_store(int(n), int(K), _ptr(obs), _ptr(action), _ptr(reward), _ptr(done), s)
     if rc != 0:
         raise ValueError(f"rlsim_probe_store rejected its arguments (status {rc})")
+
+
+def probe_policy_math(lo_bits: int, count: int, out_max, stream=None) -> None:
+    """Merge the policy functions' maximum errors over fp32 bit patterns
+    [lo_bits, lo_bits + count) into out_max (a zeroed int32 device tensor of 3;
+    read it with .view(torch.float32)); raises ValueError on a rejected argument."""
+    s = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    rc = probe_lib.rlsim_probe_policy_math(int(lo_bits), int(count), _ptr(out_max), s)
+    if rc != 0:
+        raise ValueError(f"rlsim_probe_policy_math rejected its arguments (status {rc})")

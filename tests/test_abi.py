@@ -201,3 +201,7 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.rlsim_probe_store((1 << 30) + 1, 4, 4, 4, 4, 4, None) == -1
     assert L.rlsim_probe_store(8, 4, None, 4, 4, 4, None) == -1
     assert L.rlsim_probe_store(8, 4, 6, 4, 4, 4, None) == -1     # misaligned obs
+    assert L.rlsim_probe_policy_math(0, 0, 4, None) == -1
+    assert L.rlsim_probe_policy_math(1, 1 << 32, 4, None) == -1
+    assert L.rlsim_probe_policy_math(0, 16, None, None) == -1
+    assert L.rlsim_probe_policy_math(0, 16, 6, None) == -1         # misaligned out_max

@@ -5,7 +5,12 @@ random action bit, the simulation step, the done byte (episode lengths tracked
 from the reset) and the next row -- the reset draw after an episode end -- and
 requires the recorded row to match bit for bit, for every environment and every
 step: the whole 65,536-env x 1,000-step workload in its fused and unfused forms,
-and a quarter of a million environments of the 4,194,304-env headline launch."""
+and a quarter of a million environments of the 4,194,304-env headline launch.
+The MLP-policy workload (1,048,576 envs x 256 steps in K = 16 launches) is
+checked the same way on 16,384 of its environments, every step, by
+orc_check_policy_rows: p0, log pi and the value inside the oracle's enclosures
+(tests/policy_bounds.py), the action following the recorded p0 exactly, the
+rest bit for bit."""
 import concurrent.futures as cf
 import os
 
@@ -92,3 +97,78 @@ def test_headline_launch_quarter_million_envs_every_step():
         del tr
     finally:
         sim.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_workload_16k_envs_every_step(dtype):
+    import policy_bounds
+    from test_gpu_policy import F32_P0_GATE, _device_policy
+
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C5"]
+    n, T, K, seed = w["n"], w["T"], w["K"][0], w["seed"]
+    wts = workloads.mlp_weights(seed)
+    S = 4096                                             # envs per slice, four slices
+    st, keep = _device_policy(wts, dtype)
+    sim = Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(seed)
+        tr = Trajectory(T, n, stats=False, p0=True, learner=True)
+        for k0 in range(0, T, K):
+            sim.step(K, tr.rows(k0, K), policy=st)     # the bench's launch shape
+        torch.cuda.synchronize()
+        starts = (0, n // 3 + 5, 2 * n // 3, n - S)
+        keys = ("obs", "action", "reward", "done", "policy_p0", "logp", "value")
+        cols = {key: np.concatenate([getattr(tr, key)[..., a:a + S].cpu().numpy() for a in starts], axis=-1)
+                for key in keys}
+        del tr
+    finally:
+        sim.close()
+    del keep
+    env_ids = np.concatenate([np.arange(a, a + S) for a in starts])
+    params = oracle.make_params(**workloads.CARTPOLE)
+    pol = oracle.Policy(**wts, bf16=(dtype == "bf16"))
+    errs = policy_bounds.errs()
+
+    def one(a, b):
+        # each column range lies inside one slice of consecutive env ids
+        if a == b:
+            return None
+        assert env_ids[b - 1] - env_ids[a] == b - 1 - a
+        c = {key: v[..., a:b] for key, v in cols.items()}
+        bad, first, stats = oracle.check_policy_rows(
+            params, pol, seed, int(env_ids[a]), 0, c["obs"], c["action"], c["reward"], c["done"], c["policy_p0"],
+            errs, logp=c["logp"], value=c["value"])
+        stats["width_sum"] = stats["mean_width"] * (b - a) * T
+        return bad, (None if first is None else (first[0], int(env_ids[a + first[1]]))), stats
+
+    ranges = []
+    for j in range(4):                                   # split each slice on its own
+        per = max(1, THREADS // 4)
+        edges = np.linspace(j * S, (j + 1) * S, per + 1).astype(int)
+        ranges += [(int(edges[m]), int(edges[m + 1])) for m in range(per)]
+    with cf.ThreadPoolExecutor(max_workers=THREADS) as ex:
+        res = [r for r in ex.map(lambda ab: one(*ab), ranges) if r is not None]
+    bad = sum(r[0] for r in res)
+    firsts = [r[1] for r in res if r[1] is not None]
+    worst = max(r[2]["worst"] for r in res)
+    exempt = sum(r[2]["exempt"] for r in res)
+    max_width = max(r[2]["max_width"] for r in res)
+    mean_width = sum(r[2]["width_sum"] for r in res) / (4 * S * T)
+    print(f"{dtype}: worst |p0 - oracle| {worst:.3g}, p0 enclosure width mean {mean_width:.3g} max {max_width:.3g}, "
+          f"{exempt} actions differ from the oracle's", flush=True)
+    if bad:
+        k, env = firsts[0]
+        col = int(np.nonzero(env_ids == env)[0][0])
+        logit, p_ref, v_ref = pol.eval(cols["obs"][k, :, col])
+        enc = pol.bounds(cols["obs"][k, :, col], errs)
+        a = int(cols["action"][k, col])
+        detail = dict(step=k, env=env, u=float(oracle.policy_u(seed, env, k)), action=a,
+                      p0=(float(cols["policy_p0"][k, col]), p_ref), logp=(float(cols["logp"][k, col]),
+                                                                        oracle.log_prob(logit, a)),
+                      value=(float(cols["value"][k, col]), v_ref), logits=tuple(logit), enclosures=enc)
+        raise AssertionError(f"{dtype}: {bad} failing env-steps; first {detail}; firsts {firsts[:4]}")
+    assert exempt <= 4 * S * T // 10000, exempt
+    if dtype == "f32":
+        assert worst <= F32_P0_GATE, worst
+    assert int(cols["done"].astype(bool).sum()) > 0

@@ -298,3 +298,91 @@ def test_row_checker_accepts_oracle_rows_and_finds_planted_errors(over):
     tr2 = sim.step(25)
     assert oracle.check_rows(params, seed, env0, t, tr2["obs"], tr2["action"], tr2["reward"], tr2["done"],
                              ep0=ep) == (0, None)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_policy_row_checker_accepts_oracle_rows_and_finds_planted_errors(bf16):
+    """orc_check_policy_rows passes the oracle's own policy trajectory (p0, log pi
+    and value rounded to fp32, as a device records them), accepts a recorded
+    value at the edge of its enclosure and rejects one just past it, flags a
+    planted error in the trajectory at its row and env, and admits an action
+    that differs from the oracle's only when u lies inside the p0 enclosure."""
+    import policy_bounds
+    params = oracle.make_params(**workloads.cartpole(max_episode_steps=9))
+    w = workloads.mlp_weights(7)
+    rng = np.random.Generator(np.random.PCG64(8))
+    for k in ("b1", "b2", "b3", "bv"):
+        w[k] = (rng.standard_normal(w[k].shape) * 0.3).astype(np.float32)
+    pol = oracle.Policy(**w, bf16=bf16)
+    n, T, env0, seed = 61, 40, 300, 9
+    sim = oracle.Sim(n, 0, params, env0=env0)
+    sim.reset(seed)
+    tr = sim.step(T, policy=pol)
+    f = {k: tr[k].astype(np.float32) for k in ("p0", "logp", "value")}
+    rows = dict(obs=tr["obs"], action=tr["action"], reward=tr["reward"], done=tr["done"])
+
+    def check(errs=None, **repl):
+        r = dict(rows, p0=f["p0"], logp=f["logp"], value=f["value"])
+        r.update(repl)
+        return oracle.check_policy_rows(params, pol, seed, env0, 0, r["obs"], r["action"], r["reward"], r["done"],
+                                        r["p0"], errs or policy_bounds.errs(), logp=r["logp"], value=r["value"])
+
+    bad, first, st = check()
+    assert (bad, first, st["exempt"]) == (0, None, 0) and st["worst"] <= 6e-8
+    assert 0.0 < st["mean_width"] <= st["max_width"] < 0.01
+    assert int(tr["done"].max()) >= 1                    # episode ends are crossed
+    # the enclosure's edge passes, the next float past it fails
+    u_all = np.array([[oracle.policy_u(seed, env0 + i, k) for i in range(n)] for k in range(T)])
+    gap = np.abs(u_all - tr["p0"])
+    k, i = np.unravel_index(int(np.argmax(gap)), gap.shape)      # a row where u is far from p0
+    obs_ki = tr["obs"][k, :, i]
+    b = pol.bounds(obs_ki, policy_bounds.errs())
+    a = int(tr["action"][k, i])
+    for field, (lo, hi) in (("p0", b["p0"]), ("logp", b["logp1" if a else "logp0"]), ("value", b["value"])):
+        for edge, outward in ((lo, -1.0), (hi, 1.0)):
+            inside = np.float32(edge)
+            if (float(inside) - edge) * outward > 0:                  # fp32 rounding moved it outside
+                inside = np.nextafter(inside, np.float32(-outward * 10))
+            arr = f[field].copy()
+            arr[k, i] = inside
+            assert check(**{field: arr})[0] == 0, (field, edge)
+            arr[k, i] = np.nextafter(inside, np.float32(outward * 10))
+            while (float(arr[k, i]) - edge) * outward <= 0:
+                arr[k, i] = np.nextafter(arr[k, i], np.float32(outward * 10))
+            bad, first, _ = check(**{field: arr})
+            assert bad == 1 and first == (k, i), (field, edge, bad, first)
+    for field, kk, ii in (("action", 11, 30), ("obs", 25, 7), ("reward", 2, 2), ("done", 30, 44)):
+        arr = rows[field].copy()
+        if field == "action":
+            arr[kk, ii] ^= 1
+        elif field == "obs":
+            arr[kk, 1, ii] = np.nextafter(arr[kk, 1, ii], np.float32(-1))
+        elif field == "reward":
+            arr[kk, ii] = 0.0
+        else:
+            arr[kk, ii] ^= 1
+        bad, first, _ = check(**{field: arr})
+        want_k = kk - 1 if field == "obs" else kk
+        assert bad >= 1 and first == (want_k, ii), (field, bad, first)
+    # an action flip on the last row (nothing after it to diverge): record p0
+    # just across u with the flipped action, its done byte and its log pi
+    k = T - 1
+    i = int(np.argmin(gap[k]))
+    u = float(u_all[k, i])
+    a = 1 - int(tr["action"][k, i])
+    p0g, act, done, logp = f["p0"].copy(), tr["action"].copy(), tr["done"].copy(), f["logp"].copy()
+    p0g[k, i] = np.nextafter(np.float32(u), np.float32(2)) if a == 0 else np.float32(u)
+    act[k, i] = a
+    logit, _, _ = pol.eval(tr["obs"][k, :, i])
+    post = oracle.env_step(params, tr["obs"][k, :, i], a)
+    done[k, i] = int(oracle.terminated(params, post)) | (tr["done"][k, i] & 2)    # the time limit: action-free
+    logp[k, i] = np.float32(oracle.log_prob(logit, a))
+    flip = dict(action=act, done=done, p0=p0g, logp=logp)
+    wide = policy_bounds.errs(scale=4.0 * (gap[k, i] + 1e-6) / policy_bounds.E_P0)    # enclosure holds u
+    bad, first, st = check(errs=wide, **flip)
+    assert (bad, st["exempt"]) == (0, 1), (bad, first, st, gap[k, i])
+    bad, first, st = check(**flip)                        # the true enclosure does not
+    assert (bad, first) == (1, (k, i)), (bad, first, gap[k, i])
+    # the recorded action must follow the recorded p0 exactly, whatever the enclosure
+    bad, first, _ = check(errs=wide, p0=p0g)
+    assert (bad, first) == (1, (k, i))
