@@ -24,9 +24,9 @@
  * 50-digit Euler-Lagrange solve, linearisation, conservation laws, closed
  * forms of the padding recurrence and of special MLP weights).
  *
- * At the end of the file are test helpers built on these definitions: the
- * teacher-forced row checkers, and orc_mlp_bounds, the interval enclosure of
- * a device evaluation of the policy that serves as its tolerance.
+ * Test helpers built on these definitions: orc_mlp_bounds (after the policy),
+ * the interval enclosure of a device evaluation of the policy that serves as
+ * its tolerance, and the teacher-forced row checkers (at the end).
  */
 #include <math.h>
 #include <stdint.h>
