@@ -173,7 +173,22 @@ def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
                       f"(seed {seed}, trajectory recorded) on {threads} threads, {mt_s:.1f} s wall",
             "single_thread": {"value": single, "unit": "env-steps/s", "cores": 1,
                               "sample": f"{slices} slices x {n_slice_envs} envs x {T} steps, {single_s:.1f} s"},
-            "other_workloads": cpu_other_workloads(threads)}
+            "other_workloads": cpu_other_workloads(threads), "host": host_cpu()}
+
+
+def host_cpu() -> dict:
+    """The host the oracle was timed on: CPU model, logical CPUs, and the CPUs
+    this process may run on."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
 
 
 def cpu_other_workloads(threads: int) -> dict:

@@ -67,10 +67,10 @@ def _compile(srcs: list, lib: str, verbose: bool) -> None:
     os.replace(tmp, lib)
 
 
-def asm(out_path: str) -> str:
-    """Write the gfx950 assembly of the device code (for inspection)."""
+def asm(out_path: str, src: str = SRC) -> str:
+    """Write the gfx950 assembly of a source's device code (for inspection)."""
     cmd = [HIPCC, *[f for f in FLAGS if f not in ("-shared", "-fPIC")], "-I", INCLUDE,
-           "--cuda-device-only", "-S", "-o", out_path, SRC]
+           "--cuda-device-only", "-S", "-o", out_path, src]
     subprocess.run(cmd, check=True)
     return out_path
 

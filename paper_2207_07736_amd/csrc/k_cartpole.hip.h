@@ -124,15 +124,18 @@ struct CartCore {
         const bool trunc = (p.max_steps != 0u) && (len >= p.max_steps);
         const uint32_t d = (trunc ? 2u : 0u) + (uint32_t)term;
         if (REC) {
-            // the offsets are passed through an empty asm in place each step
+            // the offsets are passed through an empty asm in place each step.
+            // Byte planes first: about 1.5 % faster than obs first.  (Forcing
+            // all seven stores back to back, the probe's fastest order, is
+            // about 11 % slower here, with the step's arithmetic around them.)
             asm volatile("" : "+v"(off4), "+v"(off1a), "+v"(off1d));
+            *at(act_row, off1a) = (uint8_t)act;
+            *at(done_row, off1d) = (uint8_t)d;
             *at(obs, off4) = s.x;
             *at(obs + plane, off4) = s.xd;
             *at(obs + 2 * plane, off4) = s.th;
             *at(obs + 3 * plane, off4) = s.thd;
-            *at(act_row, off1a) = (uint8_t)act;
             *at(rew_row, off4) = 1.0f;
-            *at(done_row, off1d) = (uint8_t)d;
         }
         const bool reset = term || trunc;
         s.x = reset ? rs.x : nx.x;

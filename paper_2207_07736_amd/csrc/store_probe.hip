@@ -1,9 +1,12 @@
 // store_probe.hip -- the probe library of include/rlsim_probe.h.  Here the
-// store-only probe: the fused kernel's trajectory stores (same planes, same
-// per-lane offsets laundered through an empty asm, same scalar row bases, same
-// workgroup mapping) with the simulation taken out.  The policy-math error
-// probe is math_probe.hip.h, included at the end (one translation unit: the
-// kernel headers define kernels).
+// store-only probe: the trajectory bytes of the fused kernel (same planes,
+// scalar row bases with per-lane offsets, same workgroup mapping) with the
+// simulation taken out.  Each step's seven stores issue back to back, byte
+// planes first: of the orders measured for these planes this one writes
+// fastest (about 6 % faster than the same stores with other instructions
+// between them), so the probe's time is the ceiling for the layout.  The
+// policy-math error probe is math_probe.hip.h, included at the end (one
+// translation unit: the kernel headers define kernels).
 #include <hip/hip_runtime.h>
 
 #include "rlsim_probe.h"
@@ -17,19 +20,23 @@ __global__ __launch_bounds__(kBlock) void k_store_probe(uint32_t n, uint32_t K, 
     const uint32_t env = xcd_block() * kBlock + threadIdx.x;
     if (env >= n) return;
     const size_t plane = n;
-    uint32_t off4 = env * 4u, off1a = env, off1d = env;
+    const uint32_t off4 = env * 4u, off1 = env;
     float v = (float)(env & 0xFFFFu);
     uint32_t bits = env;
 #pragma unroll 1
     for (uint32_t k = 0; k < K; ++k) {
-        asm volatile("" : "+v"(off4), "+v"(off1a), "+v"(off1d));
+        const float v1 = v + 1.0f, v2 = v + 2.0f, v3 = v + 3.0f;
+        const uint8_t a = (uint8_t)(bits & 1u), d = (uint8_t)((env ^ k) & 3u);
+        float* o1 = obs + plane;
+        float* o2 = obs + 2 * plane;
+        float* o3 = obs + 3 * plane;
+        *at(act, off1) = a;
+        *at(done, off1) = d;
         *at(obs, off4) = v;
-        *at(obs + plane, off4) = v + 1.0f;
-        *at(obs + 2 * plane, off4) = v + 2.0f;
-        *at(obs + 3 * plane, off4) = v + 3.0f;
-        *at(act, off1a) = (uint8_t)(bits & 1u);
+        *at(o1, off4) = v1;
+        *at(o2, off4) = v2;
+        *at(o3, off4) = v3;
         *at(rew, off4) = 1.0f;
-        *at(done, off1d) = (uint8_t)((env ^ k) & 3u);
         v += 1.0f;
         bits += 1u;
         obs += 4 * plane;

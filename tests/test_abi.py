@@ -205,3 +205,19 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.rlsim_probe_policy_math(1, 1 << 32, 4, None) == -1
     assert L.rlsim_probe_policy_math(0, 16, None, None) == -1
     assert L.rlsim_probe_policy_math(0, 16, 6, None) == -1         # misaligned out_max
+
+
+def test_probe_issues_each_steps_stores_back_to_back(tmp_path):
+    """The store probe's time is the layout's ceiling only in its fastest
+    order: the seven stores of a step with nothing between them, byte planes
+    first.  The compiler chooses the schedule, so the built assembly is read."""
+    from paper_2207_07736_amd import build
+    out = build.asm(str(tmp_path / "probe.s"), build.PROBE_SRCS[0])
+    text = open(out).read()
+    name = next(l.split(":")[0] for l in text.splitlines() if l.startswith("_ZN9rlsim_dev13k_store_probe"))
+    body = text[text.index(name + ":"):]
+    body = body[:body.index("s_endpgm")].splitlines()
+    code = [l.split()[0] for l in body if l.strip() and not l.strip().startswith((";", "."))]
+    stores = [i for i, op in enumerate(code) if op.startswith("global_store")]
+    assert len(stores) == 7 and stores[-1] - stores[0] == 6, [code[i] for i in range(stores[0], stores[-1] + 1)]
+    assert [code[i] for i in stores] == ["global_store_byte"] * 2 + ["global_store_dword"] * 5
