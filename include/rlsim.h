@@ -73,10 +73,10 @@ void rlsim_cfg_default(rlsim_cfg* cfg);
  * each (4 cart-pole words x, x_dot, theta, theta_dot, then D padding words),
  * on the current HIP device.  Allocates the state (about (20 + 12 D) bytes per
  * environment) on the device.  cfg may be NULL (defaults).
- * Errors: EINVAL if out == NULL, n_envs == 0 or n_envs > 2^30, state_words < 4,
- * a non-finite or inconsistent constant (masses <= 0, half_length <= 0,
- * reset_low > reset_high, compute_factor == 0, ...); ENOMEM; EDEVICE.  On error
- * *out is NULL. */
+ * Errors: EINVAL if out == NULL, n_envs == 0 or n_envs > 2^30, state_words < 4
+ * or state_words > 2^24 + 4, a non-finite or inconsistent constant (masses <= 0,
+ * half_length <= 0, reset_low > reset_high, compute_factor == 0, ...); ENOMEM;
+ * EDEVICE.  On error *out is NULL. */
 int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rlsim_t** out);
 
 /* Start every environment's first episode at global step t = 0 (Background,

@@ -203,8 +203,10 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
     const bool live = env < a.n;
     CartCore<REC, STATS> core(a.p, env);
     if (live) core.load(a);
-    for (uint32_t k0 = 0; k0 < a.K; k0 += kChunk) {
-        const uint32_t steps = min(kChunk, a.K - k0);
+    // k0 advances by the round's own length, so it never passes K (a K within
+    // one round of 2^32 cannot wrap it)
+    for (uint32_t k0 = 0, steps = 0; k0 < a.K; k0 += steps) {
+        steps = min(kChunk, a.K - k0);
         BitRecorder rec{lds_u, lds_d, threadIdx.x};
         if (live) {
             if (REC) core.set_rows(a, k0);

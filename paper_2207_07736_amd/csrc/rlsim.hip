@@ -163,6 +163,10 @@ unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 // Largest padding count of the register-resident (one thread per env) kernel;
 // above it the two-phase wide kernel holds the words.
 constexpr uint32_t kMaxRegisterWords = 16u;
+// Largest state: 2^24 padding words per environment (3 x 64 MiB of device
+// memory per environment), which keeps the wide kernel's 32-bit word indices
+// (row offsets, chunk counts) far from overflow.
+constexpr uint32_t kMaxStateWords = (1u << 24) + 4u;
 
 template <bool REC, bool STATS>
 hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
@@ -236,7 +240,8 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
     if (!out) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: out is NULL");
     *out = nullptr;
     if (n_envs == 0u || n_envs > (1u << 30)) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: n_envs must be in [1, 2^30]");
-    if (state_words < 4u) return fail(nullptr, RLSIM_EINVAL, "rlsim_create: state_words must be >= 4");
+    if (state_words < 4u || state_words > kMaxStateWords)
+        return fail(nullptr, RLSIM_EINVAL, "rlsim_create: state_words must be in [4, 2^24 + 4]");
     rlsim_cfg c;
     if (cfg) c = *cfg;
     else rlsim_cfg_default(&c);

@@ -60,7 +60,7 @@ def test_cfg_default_matches_workload_constants():
     assert c.stream is None
 
 
-@pytest.mark.parametrize("n,words", [(0, 4), (1 << 30 | 1, 4), (16, 3), (16, 0)])
+@pytest.mark.parametrize("n,words", [(0, 4), (1 << 30 | 1, 4), (16, 3), (16, 0), (1, (1 << 24) + 5), (1, 2**32 - 1)])
 def test_create_rejects_bad_sizes(n, words):
     import paper_2207_07736_amd as p
     with pytest.raises(p.RlsimError) as e:
