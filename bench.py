@@ -285,23 +285,7 @@ def fusion_sweeps(stream) -> dict:
                       "K100": {"ms": fused}}
     del traj
     sim.close()
-    w = workloads.WORKLOADS["C2"]
-    n, T = w["n"], w["T"]
-    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
-    sim.reset(w["seed"])
-    traj = Trajectory(T, n)
-    rows = {}
-    for K in w["K"]:
-        ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=3)
-        rows[str(K)] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3)}
-    base = rows["1"]["ms"]
-    for r in rows.values():
-        r["speedup_vs_K1"] = base / r["ms"]
-    gms = _graph_ms(sim, [traj.rows(k, 1) for k in range(T)], stream, 3)
-    rows["1_hipgraph"] = {"ms": gms, "env_steps_per_s": n * T / (gms * 1e-3), "speedup_vs_K1": base / gms}
-    out[w["name"]] = rows
-    del traj
-    sim.close()
+    out[workloads.WORKLOADS["C2"]["name"]] = k_sweep(stream)
 
     w = workloads.WORKLOADS["C4"]
     n, T = w["n"], w["T"]
@@ -355,6 +339,46 @@ def compute_factor_sweep(stream) -> dict:
     print("[bench] compute-factor sweep: " + ", ".join(f"{k} {v['fusion_speedup']:.2f}x" for k, v in rows.items()),
           file=sys.stderr, flush=True)
     return rows
+
+
+def k_sweep(stream) -> dict:
+    """Fused against unfused on the K sweep (65,536 envs x 1,000 steps, K = 1,
+    10, 100, 1,000; three timed repetitions after one warm-up each), then the
+    1,000 K = 1 launches captured in one HIP graph and replayed (one warm-up,
+    three timed)."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C2"]
+    n, T = w["n"], w["T"]
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n)
+    rows = {}
+    for K in w["K"]:
+        ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=3)
+        rows[str(K)] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3)}
+    base = rows["1"]["ms"]
+    for r in rows.values():
+        r["speedup_vs_K1"] = base / r["ms"]
+    gms = _graph_ms(sim, [traj.rows(k, 1) for k in range(T)], stream, 3)
+    rows["1_hipgraph"] = {"ms": gms, "env_steps_per_s": n * T / (gms * 1e-3), "speedup_vs_K1": base / gms}
+    del traj
+    sim.close()
+    return rows
+
+
+def sweep_only(which: str) -> int:
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    if which == "ksweep":
+        rows = {workloads.WORKLOADS["C2"]["name"]: k_sweep(stream)}
+    else:
+        rows = {workloads.C_SWEEP["name"]: compute_factor_sweep(stream)}
+    print(json.dumps(rows), flush=True)
+    return 0
 
 
 MLP_FLOPS_PER_ENV_STEP = 2 * (64 * 4 + 64 * 64 + 2 * 64)
@@ -543,7 +567,12 @@ def main() -> int:
                     help="time only the state-size workload (262,144 envs, K = 500) with D padding words")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM traffic summary from two rocprofv3 counter CSVs and exit")
+    ap.add_argument("--sweep-only", choices=("ksweep", "csweep"),
+                    help="run only the K sweep with its HIP-graph form (65,536 envs x 1,000 steps) or only "
+                         "the compute-factor sweep, print its rows as JSON (profiling)")
     args = ap.parse_args()
+    if args.sweep_only:
+        return sweep_only(args.sweep_only)
 
     if args.policy:
         return policy_only(args.policy, args.steps, args.warmup)
