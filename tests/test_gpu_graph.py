@@ -60,3 +60,50 @@ def test_graph_of_unfused_launches_matches_eager(D):
         del g, tr
     finally:
         sim.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_graph_of_policy_launches_matches_eager(dtype):
+    """The MLP-policy kernel in a graph: 8 launches of K = 4 with p0, log pi and
+    value recorded, replayed three times; every output plane equals the eager
+    run bit for bit."""
+    from test_gpu_policy import _device_policy, _weights
+
+    from paper_2207_07736_amd import Simulator, Trajectory
+    n, T, K, seed = 2000, 32, 4, 6
+    st, keep = _device_policy(_weights(21, 0.2), dtype)
+    s = torch.cuda.Stream()
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=s)
+    planes = ("obs", "action", "reward", "done", "policy_p0", "logp", "value")
+    try:
+        tr = Trajectory(T, n, p0=True, learner=True)
+        rows = [tr.rows(k0, K) for k0 in range(0, T, K)]
+        with torch.cuda.stream(s):
+            sim.reset(seed)
+            for r in rows:
+                sim.step(K, r, policy=st)
+            s.synchronize()
+            ref = {k: getattr(tr, k).clone() for k in planes}
+            ref_state = sim.get_state()
+            sim.reset(seed)
+            s.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                for r in rows:
+                    sim.step(K, r, policy=st)
+            for rep in range(3):
+                for k in planes:
+                    getattr(tr, k).zero_()
+                sim.reset(seed)
+                s.synchronize()
+                g.replay()
+                s.synchronize()
+                for k in planes:
+                    assert torch.equal(getattr(tr, k), ref[k]), (rep, k)
+                st_, ep, _ = sim.get_state()
+                assert np.array_equal(st_.view(np.uint32), ref_state[0].view(np.uint32))
+                assert np.array_equal(ep, ref_state[1])
+        del g, tr
+    finally:
+        sim.close()
+    del keep
