@@ -35,7 +35,7 @@ def test_c_client_run_matches_oracle(tmp_path, n, K, seed):
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    assert os.path.exists(EXE), "tests/c_client/rlsim_client is missing: run __graft_entry__.build()"
+    _ensure_built()                 # normally built by __graft_entry__.build(); gcc takes well under a second
     out = tmp_path / "run.bin"
     r = subprocess.run([EXE, str(n), str(K), str(seed), str(out)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr
