@@ -109,7 +109,7 @@ def ingest_pmc(fetch_csv: str, write_csv: str, workload: str, kernel_prefix: str
     path = traffic_file(workload)
     with open(path, "w") as fh:
         fh.write(f"""# HBM traffic of one launch, from rocprofv3 counters (KiB per dispatch, median)
-# commands (repository root on the GPU box, run from /tmp with TMPDIR=/tmp):
+# commands (repository root, run from /tmp with TMPDIR=/tmp):
 #   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/pmc_fetch -o f -- python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu --no-sweep --no-unfused --copy-calibration
 #   rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/pmc_write -o w -- python3 <repo>/bench.py --steps 3 --warmup 1 --no-cpu --no-sweep --no-unfused --copy-calibration
 #   python bench.py --ingest-pmc <out>/pmc_fetch/f_counter_collection.csv <out>/pmc_write/w_counter_collection.csv
