@@ -315,3 +315,14 @@ def test_policy_errors():
     finally:
         sim.close()
     del keep
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n", [1, 63, 65, 257])
+def test_policy_tiny_and_ragged_env_counts(dtype, n):
+    """Env counts that leave most of a wave's matrix columns, or a workgroup's
+    waves, empty: every recorded step still follows the teacher-forced rules."""
+    w = _weights(31, 0.2)
+    g = _gpu_policy_run(n, 24, 8, w, dtype, 13)
+    _check_teacher_forced(g, w, dtype, 13, list(range(n)))
+    assert g["t"] == 24
