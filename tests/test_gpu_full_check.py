@@ -5,7 +5,9 @@ random action bit, the simulation step, the done byte (episode lengths tracked
 from the reset) and the next row -- the reset draw after an episode end -- and
 requires the recorded row to match bit for bit, for every environment and every
 step: the whole 65,536-env x 1,000-step workload in its fused and unfused forms,
-and every environment of the 4,194,304-env headline launch.
+and every environment of the 4,194,304-env headline launch and of the
+262,144-env state-size launch (D = 4,096; the other state sizes must record the
+same trajectory).
 The MLP-policy workload (1,048,576 envs x 256 steps in K = 16 launches) is
 checked the same way on 32,768 of its environments, every step, by
 orc_check_policy_rows: p0, log pi and the value inside the oracle's enclosures
@@ -178,3 +180,35 @@ def test_policy_workload_32k_envs_every_step(dtype):
     if dtype == "f32":
         assert worst <= F32_P0_GATE, worst
     assert int(cols["done"].astype(bool).sum()) > 0
+
+
+def test_state_size_workload_every_step():
+    """262,144 envs x 500 steps in one K = 500 launch with D = 4,096 padding
+    words: every recorded step teacher-forced against the oracle.  The padding
+    words never feed back into the cart-pole, so the trajectories of D = 4, 64
+    and 512 must equal it bit for bit (compared on the device)."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.WORKLOADS["C4"]
+    n, T, seed = w["n"], w["T"], w["seed"]
+    keys = ("obs", "action", "reward", "done")
+    ref = None
+    for D in sorted(w["D"], reverse=True):
+        sim = Simulator(n, D, workloads.CARTPOLE)
+        try:
+            sim.reset(seed)
+            tr = Trajectory(T, n, stats=False)
+            sim.step(T, tr.rows(0, T))
+            torch.cuda.synchronize()
+            if ref is None:
+                ref = {key: getattr(tr, key) for key in keys}
+                S = n // 4
+                for a in range(0, n, S):
+                    cols = {key: ref[key][..., a:a + S].cpu().numpy() for key in keys}
+                    bad, first = _check_all(cols, seed, a)
+                    assert bad == 0, (D, a, bad, first)
+            else:
+                for key in keys:
+                    assert torch.equal(getattr(tr, key), ref[key]), (D, key)
+                del tr
+        finally:
+            sim.close()
