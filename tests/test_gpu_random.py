@@ -1,7 +1,11 @@
 """Randomised GPU parity: seeded draws of environment count, padding words, K
 schedule, seed and simulator constants, each run compared with the oracle bit
 for bit (trajectory, statistics, final state, counters).  The draws are fixed by
-the test's own generator seed, so every run checks the same cases."""
+the test's own generator seed, so every run checks the same cases.  The
+RLSIM_RANDOM_CASES environment variable raises the case count for a longer
+campaign (default 96)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -39,12 +43,17 @@ def _case(i):
         over["compute_factor"] = int(rng.choice([2, 3, 5]))
     if rng.random() < 0.2:
         over["reset_low"], over["reset_high"] = -0.2, 0.2
+    if rng.random() < 0.25:
+        over["gravity"] = float(np.float32(rng.uniform(0.0, 20.0)))
+        over["masspole"] = float(np.float32(rng.uniform(0.01, 1.0)))
+        over["half_length"] = float(np.float32(rng.uniform(0.1, 2.0)))
+        over["tau"] = float(np.float32(rng.uniform(0.001, 0.05)))
     if over.get("max_episode_steps") == 0 and rng.random() < 0.5:
         over["no_termination"] = 1
     return n, D, T, sched, seed, over
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(int(os.environ.get("RLSIM_RANDOM_CASES", "96"))))
 def test_random_case_bit_exact(i):
     n, D, T, sched, seed, over = _case(i)
     cfg = workloads.cartpole(**over)
