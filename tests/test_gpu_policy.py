@@ -19,6 +19,8 @@ are:
 * free-running: an environment's trajectory equals the oracle's up to its first
   action disagreement, which must be one whose u lies in the p0 enclosure.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -326,3 +328,52 @@ def test_policy_tiny_and_ragged_env_counts(dtype, n):
     g = _gpu_policy_run(n, 24, 8, w, dtype, 13)
     _check_teacher_forced(g, w, dtype, 13, list(range(n)))
     assert g["t"] == 24
+
+
+def _policy_case(i):
+    rng = np.random.Generator(np.random.PCG64(5000 + i))
+    dtype = ("f32", "bf16")[i % 2]
+    n = int(rng.choice([1, 64, 100, 257, 1000, 3000]))
+    T = int(rng.integers(1, 65))
+    cuts = sorted(set(int(c) for c in rng.integers(1, T, size=int(rng.integers(0, 4)))) if T > 1 else [])
+    bounds = [0] + cuts + [T]
+    sched = [b - a for a, b in zip(bounds[:-1], bounds[1:])]
+    w = _weights(int(rng.integers(0, 1000)), float(rng.choice([0.0, 0.3, 1.0])))
+    scale = float(rng.choice([0.25, 1.0, 3.0]))          # from nearly linear to saturated units
+    for k in ("w1", "w2", "w3", "wv"):
+        w[k] = (w[k] * scale).astype(np.float32)
+    seed = int(rng.integers(0, 2**63))
+    return dtype, n, sched, w, seed
+
+
+@pytest.mark.parametrize("i", range(int(os.environ.get("RLSIM_POLICY_CASES", "16"))))
+def test_policy_random_cases(i):
+    """Seeded draws of precision, env count, K schedule, weight scale (nearly
+    linear to saturated hidden units), biases and seed; every recorded step
+    against the oracle's enclosures with the compiled checker."""
+    import paper_2207_07736_amd as p
+    dtype, n, sched, w, seed = _policy_case(i)
+    T = sum(sched)
+    print(f"policy case {i}: {dtype} n={n} sched={sched} seed={seed}", flush=True)
+    st, keep = _device_policy(w, dtype)
+    sim = p.Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(seed)
+        tr = p.Trajectory(T, n, p0=True, learner=True)
+        k0 = 0
+        for k in sched:
+            sim.step(k, tr.rows(k0, k), policy=st)
+            k0 += k
+        torch.cuda.synchronize()
+        g = {key: getattr(tr, key).cpu().numpy() for key in ("obs", "action", "reward", "done", "policy_p0", "logp",
+                                                             "value")}
+        del tr
+    finally:
+        sim.close()
+    del keep
+    bad, first, stats = oracle.check_policy_rows(
+        oracle.make_params(**workloads.CARTPOLE), oracle.Policy(**w, bf16=(dtype == "bf16")), seed, 0, 0, g["obs"],
+        g["action"], g["reward"], g["done"], g["policy_p0"], policy_bounds.errs(), logp=g["logp"], value=g["value"])
+    assert bad == 0, (i, bad, first, stats)
+    if dtype == "f32":
+        assert stats["worst"] <= F32_P0_GATE, stats
