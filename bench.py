@@ -321,11 +321,36 @@ def fusion_sweeps(stream) -> dict:
         sim.close()
         print(f"[bench] sweep D={D}: K1 {entry['K1']['ms']:.2f} ms, K500 {entry['K500']['ms']:.2f} ms", file=sys.stderr,
               flush=True)
+    # the unfused wide launches against a plain stream of the same traffic mix
+    D = max(w["D"])
+    d_rows[f"D{D}"]["K1"]["stream_probe"] = stream_ceiling(n * D, d_rows[f"D{D}"]["K1"]["algorithmic_GBs"], stream)
     out[w["name"]] = d_rows
 
     out[workloads.WORKLOADS["C5"]["name"]] = policy_sweep(stream)
     out[workloads.C_SWEEP["name"]] = compute_factor_sweep(stream)
     return out
+
+
+def stream_ceiling(words: int, achieved_gbs: float, stream) -> dict:
+    """Time rlsim_probe_stream (read s, a, b; write s) over `words` fp32 words
+    per array, and the fraction of its rate that `achieved_gbs` reaches."""
+    import torch
+    from paper_2207_07736_amd.probe import probe_stream
+    s, a, b = (torch.zeros(words, dtype=torch.float32, device="cuda") for _ in range(3))
+    probe_stream(s, a, b, stream)
+    times = []
+    for _ in range(5):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        probe_stream(s, a, b, stream)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        times.append(start.elapsed_time(stop))
+    times.sort()
+    ms = times[len(times) // 2]
+    gbs = words * 16 / (ms * 1e-3) / 1e9
+    del s, a, b
+    return {"ms": ms, "GBs": gbs, "frac_of_stream_ceiling": achieved_gbs / gbs}
 
 
 def compute_factor_sweep(stream) -> dict:

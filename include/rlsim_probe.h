@@ -1,7 +1,8 @@
 /*
  * rlsim_probe.h -- C ABI of the measurement aids beside librlsim.so
- * (librlsim_probe.so): the store-only probe of the trajectory layout, and the
- * error probe of the policy kernel's elementwise functions.
+ * (librlsim_probe.so): the store-only probe of the trajectory layout, a
+ * read/write stream probe, and the error probe of the policy kernel's
+ * elementwise functions.
  *
  * The fused simulator kernel's unavoidable work is writing the trajectory
  * (section "Simulator Kernel Fusion": fusion removes the state round trips,
@@ -55,6 +56,16 @@ int rlsim_probe_store(uint32_t n, uint32_t K, float* obs, uint8_t* action, float
  * Errors: -1 if count == 0, lo_bits + count > 2^32, or out_max is NULL or not
  * 4-byte aligned; -3 if the launch fails. */
 int rlsim_probe_policy_math(uint32_t lo_bits, uint64_t count, uint32_t* out_max, void* stream);
+
+/* A plain stream with the traffic of one unfused step of the wide padding
+ * state (section "Simulator Complexity": each word read and written once per
+ * launch): for i < n4, s[i] <- fma(a[i], s[i], b[i]) on float4 units, each
+ * component rounded once.  s, a and b are caller-owned DEVICE arrays of n4
+ * float4 (16-byte aligned); 48 bytes are read and 16 written per float4.  Its
+ * time is the ceiling that the K = 1 wide launches are compared with.
+ * Errors: -1 if n4 == 0 or a pointer is NULL or not 16-byte aligned; -3 if the
+ * launch fails. */
+int rlsim_probe_stream(uint64_t n4, float* s, const float* a, const float* b, void* stream);
 
 #ifdef __cplusplus
 }

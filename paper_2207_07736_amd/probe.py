@@ -1,6 +1,6 @@
 """Thin ctypes binding of librlsim_probe.so (include/rlsim_probe.h): the
-store-only probe of the trajectory layout and the error probe of the policy
-kernel's elementwise functions, measurement aids.  Argument
+store-only probe of the trajectory layout, a read/write stream probe and the
+error probe of the policy kernel's elementwise functions, measurement aids.  Argument
 marshalling only; fails loudly if the library has not been built."""
 from __future__ import annotations
 
@@ -9,7 +9,7 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
-PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math")
+PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream")
 
 
 def _load():
@@ -21,6 +21,8 @@ def _load():
     L.rlsim_probe_store.restype = ctypes.c_int
     L.rlsim_probe_policy_math.argtypes = [u32, ctypes.c_uint64, vp, vp]
     L.rlsim_probe_policy_math.restype = ctypes.c_int
+    L.rlsim_probe_stream.argtypes = [ctypes.c_uint64, vp, vp, vp, vp]
+    L.rlsim_probe_stream.restype = ctypes.c_int
     return L
 
 
@@ -48,3 +50,14 @@ def probe_policy_math(lo_bits: int, count: int, out_max, stream=None) -> None:
     rc = probe_lib.rlsim_probe_policy_math(int(lo_bits), int(count), _ptr(out_max), s)
     if rc != 0:
         raise ValueError(f"rlsim_probe_policy_math rejected its arguments (status {rc})")
+
+
+def probe_stream(s, a, b, stream=None) -> None:
+    """s <- fma(a, s, b) elementwise over float32 device tensors of equal size
+    (a multiple of 4, 16-byte aligned); raises ValueError on a rejected argument."""
+    if not (s.numel() == a.numel() == b.numel()) or s.numel() % 4:
+        raise ValueError("probe_stream needs three arrays of the same size, a multiple of 4")
+    st = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    rc = probe_lib.rlsim_probe_stream(s.numel() // 4, _ptr(s), _ptr(a), _ptr(b), st)
+    if rc != 0:
+        raise ValueError(f"rlsim_probe_stream rejected its arguments (status {rc})")

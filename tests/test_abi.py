@@ -205,6 +205,9 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.rlsim_probe_policy_math(1, 1 << 32, 4, None) == -1
     assert L.rlsim_probe_policy_math(0, 16, None, None) == -1
     assert L.rlsim_probe_policy_math(0, 16, 6, None) == -1         # misaligned out_max
+    assert L.rlsim_probe_stream(0, 16, 16, 16, None) == -1
+    assert L.rlsim_probe_stream(4, None, 16, 16, None) == -1
+    assert L.rlsim_probe_stream(4, 16, 24, 16, None) == -1          # misaligned a
 
 
 def test_probe_issues_each_steps_stores_back_to_back(tmp_path):

@@ -57,3 +57,20 @@ def test_probe_headline_size():
     torch.cuda.synchronize()
     assert _expected_ok(tr, n, K) is None
     del tr
+
+
+def test_stream_probe_values():
+    """rlsim_probe_stream computes s <- fma(a, s, b) on every word.  Small
+    integers over 16 keep a * s + b exact in double, so the fp32 result must be
+    that value rounded once."""
+    import numpy as np
+    from paper_2207_07736_amd.probe import probe_stream
+    rng = np.random.Generator(np.random.PCG64(3))
+    n = 4 * 70001
+    s, a, b = (rng.integers(-1000, 1001, size=n).astype(np.float32) / np.float32(16) for _ in range(3))
+    want = (a.astype(np.float64) * s + b).astype(np.float32)
+    ts, ta, tb = (torch.from_numpy(x).cuda() for x in (s, a, b))
+    probe_stream(ts, ta, tb)
+    torch.cuda.synchronize()
+    assert np.array_equal(ts.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(ta.cpu().numpy(), a) and np.array_equal(tb.cpu().numpy(), b)
