@@ -192,12 +192,16 @@ def host_cpu() -> dict:
 
 
 def cpu_other_workloads(threads: int) -> dict:
-    """The oracle on the K-sweep workload in full (65,536 envs x 1,000 steps,
-    on `threads` threads and on one), and on bounded slices of the state-size
-    and policy workloads, one slice per thread at a time (env-steps/s;
-    trajectories recorded)."""
+    """The oracle on the 1,024-env workload in full (one thread), on the K-sweep
+    workload in full (65,536 envs x 1,000 steps, on `threads` threads and on
+    one), and on bounded slices of the state-size and policy workloads, one
+    slice per thread at a time (env-steps/s; trajectories recorded)."""
     import oracle
     out = {}
+    w = workloads.WORKLOADS["C1"]
+    sec = _oracle_slices(w["n"], [0], w["T"], w["seed"], 1)
+    out[w["name"]] = {"single_thread": {"value": w["n"] * w["T"] / sec, "unit": "env-steps/s",
+                                        "sample": f"all {w['n']} envs x {w['T']} steps on 1 thread, {sec:.3f} s"}}
     w = workloads.WORKLOADS["C2"]
     n_slice = w["n"] // threads
     starts = [i * n_slice for i in range(threads)]
