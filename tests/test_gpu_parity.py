@@ -300,3 +300,41 @@ def test_env_results_independent_of_n(D):
     # the first statistics row covers envs 0..255 in both runs
     for a, b in zip(small["stats"], big["stats"]):
         assert np.array_equal(a[0], b[0])
+
+
+def test_concurrent_handles_on_two_streams_match_solo_runs():
+    """Two handles (different sizes, padding words and seeds) stepped in
+    interleaved calls on two streams, with the streams overlapping: each
+    handle's trajectory and final state equal its solo run bit for bit (the
+    library keeps no state outside the handle)."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    specs = [(3000, 0, 11, [40, 1, 39]), (1500, 24, 12, [1] * 20 + [60])]
+    solo = [gpu_run(n, sum(sch), sch, D=D, seed=seed, stats=False) for n, D, seed, sch in specs]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    sims, trajs = [], []
+    try:
+        for (n, D, seed, sch), s in zip(specs, streams):
+            sim = Simulator(n, D, workloads.CARTPOLE, stream=s)
+            sim.reset(seed)
+            sims.append(sim)
+            trajs.append(Trajectory(sum(sch), n, stats=False))
+        torch.cuda.synchronize()
+        k0 = [0, 0]
+        queues = [list(sch) for _, _, _, sch in specs]
+        while queues[0] or queues[1]:
+            for h in (0, 1):
+                if queues[h]:
+                    k = queues[h].pop(0)
+                    sims[h].step(k, trajs[h].rows(k0[h], k))
+                    k0[h] += k
+        torch.cuda.synchronize()
+        for h in (0, 1):
+            got = {key: getattr(trajs[h], key).cpu().numpy() for key in ("obs", "action", "reward", "done")}
+            state, ep, t = sims[h].get_state()
+            got.update(state=state, ep=ep, t=t)
+            for key in ("obs", "action", "reward", "done", "state", "ep"):
+                assert np.array_equal(np.asarray(got[key]).view(np.uint8), np.asarray(solo[h][key]).view(np.uint8)), (h, key)
+            assert got["t"] == solo[h]["t"]
+    finally:
+        for sim in sims:
+            sim.close()
