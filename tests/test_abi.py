@@ -224,3 +224,36 @@ def test_probe_issues_each_steps_stores_back_to_back(tmp_path):
     stores = [i for i, op in enumerate(code) if op.startswith("global_store")]
     assert len(stores) == 7 and stores[-1] - stores[0] == 6, [code[i] for i in range(stores[0], stores[-1] + 1)]
     assert [code[i] for i in stores] == ["global_store_byte"] * 2 + ["global_store_dword"] * 5
+
+
+def test_create_rejects_every_invalid_cfg_drawn():
+    """Seeded draws of configurations that break one rule each (a non-finite
+    constant, a non-positive mass, length or step, an inverted range, an
+    unknown flag, a zero compute factor): rlsim_create returns EINVAL with a
+    message and touches no device."""
+    import math
+    import paper_2207_07736_amd as p
+    rng = np.random.Generator(np.random.PCG64(77))
+    floats = ["gravity", "masscart", "masspole", "half_length", "force_mag", "tau", "x_threshold",
+              "theta_threshold_rad", "reset_low", "reset_high", "pad_a_low", "pad_a_high", "pad_b_low", "pad_b_high"]
+    for _ in range(300):
+        c = p.rlsim_cfg_default()
+        kind = int(rng.integers(0, 6))
+        if kind == 0:
+            setattr(c, floats[int(rng.integers(len(floats)))], float(rng.choice([math.nan, math.inf, -math.inf])))
+        elif kind == 1:
+            setattr(c, str(rng.choice(["masscart", "masspole", "half_length", "tau"])), -float(rng.uniform(0, 5)))
+        elif kind == 2:
+            lo, hi = str(rng.choice(["reset", "pad_a", "pad_b"])) + "_low", None
+            hi = lo.replace("_low", "_high")
+            setattr(c, lo, getattr(c, hi) + float(rng.uniform(0.01, 3)))
+        elif kind == 3:
+            c.flags = int(rng.integers(2, 2**32))
+        elif kind == 4:
+            c.compute_factor = 0
+        else:
+            c.masscart = 0.0
+        h = ctypes.c_void_p()
+        rc = p.lib.rlsim_create(16, 4, ctypes.byref(c), ctypes.byref(h))
+        assert rc == p.RLSIM_EINVAL and not h.value, (kind, rc)
+        assert p.rlsim_last_error(None).startswith("rlsim_create: cfg")
