@@ -81,3 +81,34 @@ def assert_bit_equal(gpu, ref, keys=("obs", "action", "reward", "done", "state",
             raise AssertionError(f"{key} differs first at {tuple(idx)}: gpu {g[tuple(idx)]!r} oracle {r[tuple(idx)]!r} "
                                  f"({int((~same).sum())} of {same.size} differ)")
     assert gpu["t"] == ref["t"]
+
+
+# fp32 policy: a fixed gate on |p0_gpu - p0_oracle| kept beside the derived
+# enclosure (observed differences are ~2e-7), so a defect smaller than the
+# enclosure still shows
+F32_P0_GATE = 1e-5
+
+
+def policy_weights(seed, bias_scale=0.0):
+    """The policy workload's weights from `seed`, with biases drawn at
+    `bias_scale` when it is nonzero."""
+    w = workloads.mlp_weights(seed)
+    if bias_scale:
+        rng = np.random.Generator(np.random.PCG64(seed + 1))
+        for k in ("b1", "b2", "b3", "bv"):
+            w[k] = (rng.standard_normal(w[k].shape) * bias_scale).astype(np.float32)
+    return w
+
+
+def device_policy(w, dtype):
+    """rlsim_policy for weights `w` as device tensors in `dtype` ("f32" or
+    "bf16"); returns (struct, tensors to keep alive)."""
+    import paper_2207_07736_amd as p
+    import torch
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = {k: torch.from_numpy(w[k]).to("cuda") for k in w}
+    tens = {k: dev[k].to(tdt).contiguous() for k in ("w1", "w2", "w3", "wv") if k in dev}
+    tens.update({k: dev[k].contiguous() for k in ("b1", "b2", "b3", "bv") if k in dev})
+    st = p.policy_struct(p.RLSIM_BF16 if dtype == "bf16" else p.RLSIM_F32, tens["w1"], tens["b1"], tens["w2"],
+                         tens["b2"], tens["w3"], tens["b3"], tens.get("wv"), tens.get("bv"))
+    return st, tens

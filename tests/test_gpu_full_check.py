@@ -110,14 +110,14 @@ def test_headline_launch_every_env_every_step():
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_workload_32k_envs_every_step(dtype):
     import policy_bounds
-    from test_gpu_policy import F32_P0_GATE, _device_policy
+    from gpu_helpers import F32_P0_GATE, device_policy
 
     from paper_2207_07736_amd import Simulator, Trajectory
     w = workloads.WORKLOADS["C5"]
     n, T, K, seed = w["n"], w["T"], w["K"][0], w["seed"]
     wts = workloads.mlp_weights(seed)
     S = 8192                                             # envs per slice, four slices
-    st, keep = _device_policy(wts, dtype)
+    st, keep = device_policy(wts, dtype)
     sim = Simulator(n, 0, workloads.CARTPOLE)
     try:
         sim.reset(seed)

@@ -67,11 +67,11 @@ def test_graph_of_policy_launches_matches_eager(dtype):
     """The MLP-policy kernel in a graph: 8 launches of K = 4 with p0, log pi and
     value recorded, replayed three times; every output plane equals the eager
     run bit for bit."""
-    from test_gpu_policy import _device_policy, _weights
+    from gpu_helpers import device_policy, policy_weights
 
     from paper_2207_07736_amd import Simulator, Trajectory
     n, T, K, seed = 2000, 32, 4, 6
-    st, keep = _device_policy(_weights(21, 0.2), dtype)
+    st, keep = device_policy(policy_weights(21, 0.2), dtype)
     s = torch.cuda.Stream()
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=s)
     planes = ("obs", "action", "reward", "done", "policy_p0", "logp", "value")

@@ -27,11 +27,10 @@ import pytest
 import oracle
 import policy_bounds
 import workloads
+from gpu_helpers import F32_P0_GATE, device_policy, policy_weights
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
-
-F32_P0_GATE = 1e-5
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -41,31 +40,11 @@ def _need_gpu():
     import paper_2207_07736_amd  # noqa: F401
 
 
-def _weights(seed, bias_scale=0.0):
-    w = workloads.mlp_weights(seed)
-    if bias_scale:
-        rng = np.random.Generator(np.random.PCG64(seed + 1))
-        for k in ("b1", "b2", "b3", "bv"):
-            w[k] = (rng.standard_normal(w[k].shape) * bias_scale).astype(np.float32)
-    return w
-
-
-def _device_policy(w, dtype):
-    import paper_2207_07736_amd as p
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    dev = {k: torch.from_numpy(w[k]).to("cuda") for k in w}
-    tens = {k: dev[k].to(tdt).contiguous() for k in ("w1", "w2", "w3", "wv") if k in dev}
-    tens.update({k: dev[k].contiguous() for k in ("b1", "b2", "b3", "bv") if k in dev})
-    st = p.policy_struct(p.RLSIM_BF16 if dtype == "bf16" else p.RLSIM_F32, tens["w1"], tens["b1"], tens["w2"],
-                         tens["b2"], tens["w3"], tens["b3"], tens.get("wv"), tens.get("bv"))
-    return st, tens
-
-
 def _gpu_policy_run(n, T, K, w, dtype, seed, cfg=None, slices=None, learner=None):
     import paper_2207_07736_amd as p
     if learner is None:
         learner = "wv" in w
-    st, keep = _device_policy(w, dtype)
+    st, keep = device_policy(w, dtype)
     sim = p.Simulator(n, 0, cfg or workloads.CARTPOLE)
     try:
         sim.reset(seed)
@@ -136,7 +115,7 @@ def _check_teacher_forced(g, w, dtype, seed, env_ids, cfg=None):
 @pytest.mark.parametrize("bias_scale", [0.0, 0.3])
 def test_policy_teacher_forced(dtype, bias_scale):
     n, T, K, seed = 300, 64, 16, 5
-    w = _weights(11, bias_scale)
+    w = policy_weights(11, bias_scale)
     g = _gpu_policy_run(n, T, K, w, dtype, seed)
     worst, exempt = _check_teacher_forced(g, w, dtype, seed, list(range(n)))
     assert worst > 0.0 or dtype == "f32"
@@ -152,7 +131,7 @@ def test_policy_teacher_forced(dtype, bias_scale):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_free_running_until_exempt_divergence(dtype):
     n, T, K, seed = 256, 48, 16, 2
-    w = _weights(3)
+    w = policy_weights(3)
     g = _gpu_policy_run(n, T, K, w, dtype, seed)
     sim = oracle.Sim(n, 0, oracle.make_params(**workloads.CARTPOLE))
     sim.reset(seed)
@@ -217,7 +196,7 @@ def test_policy_without_value_head_or_learner_outputs(dtype):
     """No value head, or no learner planes: p0 and the trajectory are what they
     are with them (the extra outputs change nothing else)."""
     n, T, K, seed = 300, 32, 16, 4
-    w = _weights(12, 0.3)
+    w = policy_weights(12, 0.3)
     full = _gpu_policy_run(n, T, K, w, dtype, seed, learner=True)
     bare = _gpu_policy_run(n, T, K, w, dtype, seed, learner=False)
     nov = {k: v for k, v in w.items() if k not in ("wv", "bv")}
@@ -235,8 +214,8 @@ def test_learner_batch_is_zero_copy_and_consistent():
     learner is 1)."""
     import paper_2207_07736_amd as p
     n, T, K, seed = 4096, 64, 16, 3
-    w = _weights(5, 0.3)
-    st, keep = _device_policy(w, "f32")
+    w = policy_weights(5, 0.3)
+    st, keep = device_policy(w, "f32")
     sim = p.Simulator(n, 0, workloads.CARTPOLE)
     try:
         sim.reset(seed)
@@ -269,7 +248,7 @@ def test_policy_env_results_independent_of_n(dtype):
     """The MLP mixes 64 environments per wave in its matrix tiles, but each
     environment's outputs are its own column: the first 300 environments of a
     1,000-env run equal a 300-env run bit for bit (p0, log pi, value, actions)."""
-    w = _weights(4, 0.3)
+    w = policy_weights(4, 0.3)
     small = _gpu_policy_run(300, 32, 16, w, dtype, 6)
     big = _gpu_policy_run(1000, 32, 16, w, dtype, 6, slices=[(0, 300)])
     for k in ("obs", "action", "done", "p0", "logp", "value"):
@@ -279,7 +258,7 @@ def test_policy_env_results_independent_of_n(dtype):
 def test_policy_errors():
     import paper_2207_07736_amd as p
     w = workloads.mlp_weights(0)
-    st, keep = _device_policy(w, "f32")
+    st, keep = device_policy(w, "f32")
     sim = p.Simulator(100, 2, workloads.CARTPOLE)
     try:
         sim.reset(0)
@@ -324,7 +303,7 @@ def test_policy_errors():
 def test_policy_tiny_and_ragged_env_counts(dtype, n):
     """Env counts that leave most of a wave's matrix columns, or a workgroup's
     waves, empty: every recorded step still follows the teacher-forced rules."""
-    w = _weights(31, 0.2)
+    w = policy_weights(31, 0.2)
     g = _gpu_policy_run(n, 24, 8, w, dtype, 13)
     _check_teacher_forced(g, w, dtype, 13, list(range(n)))
     assert g["t"] == 24
@@ -338,7 +317,7 @@ def _policy_case(i):
     cuts = sorted(set(int(c) for c in rng.integers(1, T, size=int(rng.integers(0, 4)))) if T > 1 else [])
     bounds = [0] + cuts + [T]
     sched = [b - a for a, b in zip(bounds[:-1], bounds[1:])]
-    w = _weights(int(rng.integers(0, 1000)), float(rng.choice([0.0, 0.3, 1.0])))
+    w = policy_weights(int(rng.integers(0, 1000)), float(rng.choice([0.0, 0.3, 1.0])))
     scale = float(rng.choice([0.25, 1.0, 3.0]))          # from nearly linear to saturated units
     for k in ("w1", "w2", "w3", "wv"):
         w[k] = (w[k] * scale).astype(np.float32)
@@ -355,7 +334,7 @@ def test_policy_random_cases(i):
     dtype, n, sched, w, seed = _policy_case(i)
     T = sum(sched)
     print(f"policy case {i}: {dtype} n={n} sched={sched} seed={seed}", flush=True)
-    st, keep = _device_policy(w, dtype)
+    st, keep = device_policy(w, dtype)
     sim = p.Simulator(n, 0, workloads.CARTPOLE)
     try:
         sim.reset(seed)
