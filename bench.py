@@ -159,7 +159,7 @@ def cpu_baseline(n_slice_envs: int, slices: int, T: int, seed: int) -> dict:
     the paper's multi-core C++ simulator baseline divides environments over
     cores) and single-threaded."""
     import oracle  # noqa: F401  (builds the oracle before any timing)
-    n_total = workloads.WORKLOADS["C3"]["n"]
+    n_total = workloads.WORKLOADS[workloads.HEADLINE]["n"]
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
     single_starts = [i * (n_total // slices) for i in range(slices)]
     single_s = _oracle_slices(n_slice_envs, single_starts, T, seed, 1)
@@ -198,11 +198,11 @@ def cpu_other_workloads(threads: int) -> dict:
     slice per thread at a time (env-steps/s; trajectories recorded)."""
     import oracle
     out = {}
-    w = workloads.WORKLOADS["C1"]
+    w = workloads.WORKLOADS[workloads.SMALL]
     sec = _oracle_slices(w["n"], [0], w["T"], w["seed"], 1)
     out[w["name"]] = {"single_thread": {"value": w["n"] * w["T"] / sec, "unit": "env-steps/s",
                                         "sample": f"all {w['n']} envs x {w['T']} steps on 1 thread, {sec:.3f} s"}}
-    w = workloads.WORKLOADS["C2"]
+    w = workloads.WORKLOADS[workloads.K_SWEEP]
     n_slice = w["n"] // threads
     starts = [i * n_slice for i in range(threads)]
     sec = _oracle_slices(n_slice, starts, w["T"], w["seed"], threads)
@@ -211,7 +211,7 @@ def cpu_other_workloads(threads: int) -> dict:
                                   "sample": f"all {w['n']} envs x {w['T']} steps on {threads} threads, {sec:.1f} s"},
                       "single_thread": {"value": w["n"] * w["T"] / sec1, "unit": "env-steps/s",
                                         "sample": f"all {w['n']} envs x {w['T']} steps on 1 thread, {sec1:.1f} s"}}
-    w = workloads.WORKLOADS["C4"]
+    w = workloads.WORKLOADS[workloads.STATE_SWEEP]
     rows = {}
     for D in w["D"]:
         n_total = max(4096, min(65536, (1 << 24) // D))       # about 1-3 s of oracle work per D
@@ -221,7 +221,7 @@ def cpu_other_workloads(threads: int) -> dict:
         rows[f"D{D}"] = {"value": n_slice * threads * w["T"] / sec, "unit": "env-steps/s",
                          "sample": f"{threads} slices x {n_slice} envs x {w['T']} steps, {sec:.1f} s wall"}
     out[w["name"]] = rows
-    w = workloads.WORKLOADS["C5"]
+    w = workloads.WORKLOADS[workloads.MLP]
     rows = {}
     for dtype, n_total, T in (("f32", 16384, w["T"]), ("bf16", 4096, 64)):
         pol = oracle.Policy(**workloads.mlp_weights(w["seed"]), bf16=(dtype == "bf16"))
@@ -286,7 +286,7 @@ def fusion_sweeps(stream) -> dict:
     state-size sweep (262,144 envs x 500 steps, D padding words per env)."""
     from paper_2207_07736_amd import Simulator, Trajectory
     out = {}
-    w = workloads.WORKLOADS["C1"]
+    w = workloads.WORKLOADS[workloads.SMALL]
     n, T = w["n"], w["T"]
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
     sim.reset(w["seed"])
@@ -300,9 +300,9 @@ def fusion_sweeps(stream) -> dict:
                       "K100": {"ms": fused}}
     del traj
     sim.close()
-    out[workloads.WORKLOADS["C2"]["name"]] = k_sweep(stream)
+    out[workloads.WORKLOADS[workloads.K_SWEEP]["name"]] = k_sweep(stream)
 
-    w = workloads.WORKLOADS["C4"]
+    w = workloads.WORKLOADS[workloads.STATE_SWEEP]
     n, T = w["n"], w["T"]
     d_rows = {}
     for D in w["D"]:
@@ -330,7 +330,7 @@ def fusion_sweeps(stream) -> dict:
     d_rows[f"D{D}"]["K1"]["stream_probe"] = stream_ceiling(n * D, d_rows[f"D{D}"]["K1"]["algorithmic_GBs"], stream)
     out[w["name"]] = d_rows
 
-    out[workloads.WORKLOADS["C5"]["name"]] = policy_sweep(stream)
+    out[workloads.WORKLOADS[workloads.MLP]["name"]] = policy_sweep(stream)
     out[workloads.C_SWEEP["name"]] = compute_factor_sweep(stream)
     return out
 
@@ -387,7 +387,7 @@ def k_sweep(stream) -> dict:
     1,000 K = 1 launches captured in one HIP graph and replayed (one warm-up,
     three timed)."""
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C2"]
+    w = workloads.WORKLOADS[workloads.K_SWEEP]
     n, T = w["n"], w["T"]
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
     sim.reset(w["seed"])
@@ -414,7 +414,7 @@ def sweep_only(which: str) -> int:
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     if which == "ksweep":
-        rows = {workloads.WORKLOADS["C2"]["name"]: k_sweep(stream)}
+        rows = {workloads.WORKLOADS[workloads.K_SWEEP]["name"]: k_sweep(stream)}
     else:
         rows = {workloads.C_SWEEP["name"]: compute_factor_sweep(stream)}
     print(json.dumps(rows), flush=True)
@@ -429,7 +429,7 @@ def policy_only(dtype: str, steps: int, warmup: int) -> int:
     the 256 steps of 1,048,576 envs in 16 launches of K = 16."""
     import torch
     from paper_2207_07736_amd import RLSIM_BF16, RLSIM_F32, Simulator, Trajectory, policy_struct
-    w = workloads.WORKLOADS["C5"]
+    w = workloads.WORKLOADS[workloads.MLP]
     n, T, K = w["n"], w["T"], w["K"][0]
     stream = torch.cuda.current_stream()
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -467,7 +467,7 @@ def wide_only(D: int, steps: int, warmup: int) -> int:
     262,144 envs x 500 steps with D padding words, trajectory recorded."""
     import torch
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C4"]
+    w = workloads.WORKLOADS[workloads.STATE_SWEEP]
     n, T = w["n"], w["T"]
     stream = torch.cuda.current_stream()
     sim = Simulator(n, D, workloads.CARTPOLE, stream=stream)
@@ -500,7 +500,7 @@ def unfused_only(steps: int, warmup: int, copy_calibration: bool) -> int:
     read from and written to HBM at every step."""
     import torch
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
     stream = torch.cuda.current_stream()
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
@@ -541,7 +541,7 @@ def policy_sweep(stream) -> dict:
     recorded."""
     from paper_2207_07736_amd import RLSIM_BF16, RLSIM_F32, Simulator, Trajectory, policy_struct
     import torch
-    w = workloads.WORKLOADS["C5"]
+    w = workloads.WORKLOADS[workloads.MLP]
     n, T = w["n"], w["T"]
     wts = workloads.mlp_weights(w["seed"])
     rows = {}
@@ -622,7 +622,7 @@ def main() -> int:
         return unfused_only(args.steps, args.warmup, args.copy_calibration)
 
     if args.ingest_pmc:
-        w = workloads.WORKLOADS["C3"]
+        w = workloads.WORKLOADS[workloads.HEADLINE]
         print(ingest_pmc(args.ingest_pmc[0], args.ingest_pmc[1], w["name"], "void rlsim_dev::k_cartpole_fused<0"))
         return 0
 
@@ -639,7 +639,7 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T, K = w["n"], w["T"], w["K"][0]
     seed = w["seed"]
     # one side stream for every launch and every timing event (graph capture

@@ -75,7 +75,7 @@ def _check_all(tr, seed, env0):
 
 @pytest.mark.parametrize("K", [1000, 1])
 def test_k_sweep_workload_every_step(K):
-    w = workloads.WORKLOADS["C2"]
+    w = workloads.WORKLOADS[workloads.K_SWEEP]
     tr = _run(w["n"], w["T"], K, w["seed"])
     bad, first = _check_all(tr, w["seed"], 0)
     assert bad == 0, (K, bad, first)
@@ -86,7 +86,7 @@ def test_headline_launch_every_env_every_step():
     """All 4,194,304 x 200 env-steps of the bench's single K = 200 launch,
     checked in sixteen slices of 262,144 environments."""
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
     sim = Simulator(n, 0, workloads.CARTPOLE)
     try:
@@ -113,7 +113,7 @@ def test_policy_workload_32k_envs_every_step(dtype):
     from gpu_helpers import F32_P0_GATE, device_policy
 
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C5"]
+    w = workloads.WORKLOADS[workloads.MLP]
     n, T, K, seed = w["n"], w["T"], w["K"][0], w["seed"]
     wts = workloads.mlp_weights(seed)
     S = 8192                                             # envs per slice, four slices
@@ -188,7 +188,7 @@ def test_state_size_workload_every_step():
     words never feed back into the cart-pole, so the trajectories of D = 4, 64
     and 512 must equal it bit for bit (compared on the device)."""
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C4"]
+    w = workloads.WORKLOADS[workloads.STATE_SWEEP]
     n, T, seed = w["n"], w["T"], w["seed"]
     keys = ("obs", "action", "reward", "done")
     ref = None

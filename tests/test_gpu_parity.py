@@ -32,7 +32,7 @@ def _stats_equal(g, r):
 
 def test_c1_full_bit_exact():
     """1,024 envs, 100 steps, one launch per step (the unfused form), seed 0."""
-    w = workloads.WORKLOADS["C1"]
+    w = workloads.WORKLOADS[workloads.SMALL]
     sched = [1] * w["T"]
     g = gpu_run(w["n"], w["T"], sched, seed=w["seed"])
     r = oracle_run(w["n"], w["T"], sched, seed=w["seed"])
@@ -89,7 +89,7 @@ def test_edge_configs(overrides):
 def test_c2_k_sweep_full_size():
     """65,536 envs x 1,000 steps: K = 1, 10, 100 and 1,000 give the identical
     trajectory; sampled slices equal the oracle."""
-    w = workloads.WORKLOADS["C2"]
+    w = workloads.WORKLOADS[workloads.K_SWEEP]
     n, T = w["n"], w["T"]
     slices = [(0, 256), (30000, 30100), (n - 256, n)]
     outs = {K: gpu_run(n, T, [K] * (T // K), seed=w["seed"], slices=slices) for K in w["K"]}
@@ -105,7 +105,7 @@ def test_c2_k_sweep_full_size():
 
 def test_c3_headline_sampled_and_properties():
     """4,194,304 envs x 200 steps in one launch (K = 200), as the bench times it."""
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
     slices = [(0, 256), (2097152, 2097152 + 256), (n - 512, n)]
     g = gpu_run(n, T, [T], seed=w["seed"], slices=slices)
@@ -125,7 +125,7 @@ def test_c3_whole_batch_properties():
     reward is 1, actions are bits, done bytes are in {0..3}, the block statistics
     count exactly the done bytes, and stored episode counters stay below 500."""
     from paper_2207_07736_amd import Simulator, Trajectory
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
     sim = Simulator(n, 0, workloads.CARTPOLE)
     try:

@@ -178,7 +178,7 @@ def test_policy_zero_weights_is_coin_flip():
 def test_c5_full_size_sampled(dtype):
     """1,048,576 envs x 256 steps in 16 launches of K = 16 (the bench shape):
     teacher-forced checks on sampled slices, properties on the whole batch."""
-    w = workloads.WORKLOADS["C5"]
+    w = workloads.WORKLOADS[workloads.MLP]
     n, T, K, seed = w["n"], w["T"], w["K"][0], w["seed"]
     wts = workloads.mlp_weights(seed)
     slices = [(0, 64), (n - 64, n)]

@@ -48,7 +48,7 @@ def test_probe_values_ragged(n, K):
 def test_probe_headline_size():
     from paper_2207_07736_amd import Trajectory
     from paper_2207_07736_amd.probe import probe_store
-    w = workloads.WORKLOADS["C3"]
+    w = workloads.WORKLOADS[workloads.HEADLINE]
     n, K = w["n"], w["T"]
     tr = Trajectory(K, n, stats=False)
     tr.done.fill_(9)

@@ -72,12 +72,12 @@ def test_wide_set_state_round_trip():
         sim.close()
 
 
-@pytest.mark.parametrize("D", workloads.WORKLOADS["C4"]["D"])
+@pytest.mark.parametrize("D", workloads.WORKLOADS[workloads.STATE_SWEEP]["D"])
 def test_c4_full_size_fused_equals_unfused(D):
     """262,144 envs x 500 steps: one K=500 launch equals 500 K=1 launches bit for
     bit (trajectory on sampled slices, the full final state), and the sampled
     slices equal the oracle."""
-    w = workloads.WORKLOADS["C4"]
+    w = workloads.WORKLOADS[workloads.STATE_SWEEP]
     n, T = w["n"], w["T"]
     slices = [(0, 256), (n - 256, n)]
     fused = gpu_run(n, T, [T], D=D, seed=w["seed"], slices=slices)

@@ -51,14 +51,20 @@ def cartpole(**overrides) -> dict:
     return d
 
 
-# The five workloads.  n: environments, T: steps per run, K: fused steps per
-# launch (several values = a sweep), D: padding words per environment.
+# The five workloads, keyed by name.  n: environments, T: steps per run, K:
+# fused steps per launch (several values = a sweep), D: padding words per
+# environment.
+SMALL = "cartpole-1k-100-K1"              # correctness size, launch-bound
+K_SWEEP = "cartpole-64k-1000-Ksweep"      # fused steps per launch 1 .. 1,000
+HEADLINE = "cartpole-4M-200-K200"         # 4,194,304 envs x 200 steps in one launch
+STATE_SWEEP = "cartpole-256k-500-Dsweep"  # padding words D = 4 .. 4,096
+MLP = "cartpole-1M-256-K16-mlp"           # the fused MLP policy, fp32 and bf16
 WORKLOADS = {
-    "C1": dict(name="cartpole-1k-100-K1", n=1024, T=100, K=[1], D=[0], seed=0, policy=None),
-    "C2": dict(name="cartpole-64k-1000-Ksweep", n=65536, T=1000, K=[1, 10, 100, 1000], D=[0], seed=0, policy=None),
-    "C3": dict(name="cartpole-4M-200-K200", n=4194304, T=200, K=[200], D=[0], seed=0, policy=None),
-    "C4": dict(name="cartpole-256k-500-Dsweep", n=262144, T=500, K=[1, 500], D=[4, 64, 512, 4096], seed=0, policy=None),
-    "C5": dict(name="cartpole-1M-256-K16-mlp", n=1048576, T=256, K=[16], D=[0], seed=0, policy=("f32", "bf16")),
+    SMALL: dict(name=SMALL, n=1024, T=100, K=[1], D=[0], seed=0, policy=None),
+    K_SWEEP: dict(name=K_SWEEP, n=65536, T=1000, K=[1, 10, 100, 1000], D=[0], seed=0, policy=None),
+    HEADLINE: dict(name=HEADLINE, n=4194304, T=200, K=[200], D=[0], seed=0, policy=None),
+    STATE_SWEEP: dict(name=STATE_SWEEP, n=262144, T=500, K=[1, 500], D=[4, 64, 512, 4096], seed=0, policy=None),
+    MLP: dict(name=MLP, n=1048576, T=256, K=[16], D=[0], seed=0, policy=("f32", "bf16")),
 }
 
 # Compute-factor sweep (the paper's "Simulator Complexity", factor C): C Euler
