@@ -30,7 +30,7 @@ def _stats_equal(g, r):
         assert np.array_equal(a, b)
 
 
-def test_c1_full_bit_exact():
+def test_small_workload_full_bit_exact():
     """1,024 envs, 100 steps, one launch per step (the unfused form), seed 0."""
     w = workloads.WORKLOADS[workloads.SMALL]
     sched = [1] * w["T"]
@@ -86,7 +86,7 @@ def test_edge_configs(overrides):
     _stats_equal(g["stats"], r["stats"])
 
 
-def test_c2_k_sweep_full_size():
+def test_k_sweep_workload_full_size():
     """65,536 envs x 1,000 steps: K = 1, 10, 100 and 1,000 give the identical
     trajectory; sampled slices equal the oracle."""
     w = workloads.WORKLOADS[workloads.K_SWEEP]
@@ -103,7 +103,7 @@ def test_c2_k_sweep_full_size():
     assert_bit_equal(base, merged)
 
 
-def test_c3_headline_sampled_and_properties():
+def test_headline_sampled_and_properties():
     """4,194,304 envs x 200 steps in one launch (K = 200), as the bench times it."""
     w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
@@ -120,7 +120,7 @@ def test_c3_headline_sampled_and_properties():
     assert np.array_equal(g["stats"][0][blocks], want)
 
 
-def test_c3_whole_batch_properties():
+def test_headline_whole_batch_properties():
     """Properties of the full headline trajectory that hold at any size: every
     reward is 1, actions are bits, done bytes are in {0..3}, the block statistics
     count exactly the done bytes, and stored episode counters stay below 500."""

@@ -175,7 +175,7 @@ def test_policy_zero_weights_is_coin_flip():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_c5_full_size_sampled(dtype):
+def test_policy_workload_full_size_sampled(dtype):
     """1,048,576 envs x 256 steps in 16 launches of K = 16 (the bench shape):
     teacher-forced checks on sampled slices, properties on the whole batch."""
     w = workloads.WORKLOADS[workloads.MLP]

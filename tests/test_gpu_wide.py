@@ -73,7 +73,7 @@ def test_wide_set_state_round_trip():
 
 
 @pytest.mark.parametrize("D", workloads.WORKLOADS[workloads.STATE_SWEEP]["D"])
-def test_c4_full_size_fused_equals_unfused(D):
+def test_state_size_workload_fused_equals_unfused(D):
     """262,144 envs x 500 steps: one K=500 launch equals 500 K=1 launches bit for
     bit (trajectory on sampled slices, the full final state), and the sampled
     slices equal the oracle."""
