@@ -241,6 +241,44 @@ def test_nan_state_propagates_like_oracle():
         sim.close()
 
 
+@pytest.mark.parametrize("D", [0, 4, 100])
+def test_last_steps_below_the_global_step_limit(D):
+    """The final K steps before the global step reaches 2^32 - 1: the Philox
+    counter blocks (t >> 3, t >> 7) take their largest values and nothing wraps;
+    one further step is rejected.  Episode counters near the time limit make the
+    truncation path run there too."""
+    import oracle
+    from paper_2207_07736_amd import RLSIM_EINVAL, RlsimError, Simulator, Trajectory
+    n, K, seed = 300, 40, (1 << 40) + 7
+    t_start = (1 << 32) - 1 - K
+    sim = Simulator(n, D, workloads.CARTPOLE)
+    osim = oracle.Sim(n, D, oracle.make_params(**workloads.CARTPOLE))
+    try:
+        sim.reset(seed)
+        osim.reset(seed)
+        st, ep, _ = sim.get_state()
+        ep = np.random.default_rng(5).integers(0, 500, n).astype(np.uint32)
+        sim.set_state(st, ep, t_start)
+        osim.set_state(st, ep, t_start)
+        tr = Trajectory(K, n)
+        sim.step(K, tr.rows(0, K))
+        torch.cuda.synchronize()
+        ref = osim.step(K)
+        for key in ("obs", "action", "reward", "done"):
+            g = getattr(tr, key).cpu().numpy()
+            assert np.array_equal(g.view(np.uint8), ref[key].view(np.uint8)), key
+        assert (tr.done.cpu().numpy() & 2).any()
+        g_st, g_ep, g_t = sim.get_state()
+        r_st, r_ep, r_t = osim.get_state()
+        assert np.array_equal(g_st.view(np.uint32), r_st.view(np.uint32))
+        assert np.array_equal(g_ep, r_ep) and g_t == r_t == (1 << 32) - 1
+        with pytest.raises(RlsimError) as e:
+            sim.step(1)
+        assert e.value.code == RLSIM_EINVAL
+    finally:
+        sim.close()
+
+
 @pytest.mark.parametrize("C", [2, 7, 64])
 def test_compute_factor_bit_exact(C):
     """The paper's compute factor: C Euler iterations of tau / C per step."""

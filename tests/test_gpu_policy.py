@@ -356,3 +356,51 @@ def test_policy_random_cases(i):
     assert bad == 0, (i, bad, first, stats)
     if dtype == "f32":
         assert stats["worst"] <= F32_P0_GATE, stats
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_last_steps_below_the_global_step_limit(dtype):
+    """The policy kernel's final K steps before the global step reaches
+    2^32 - 1 (the sampling uniforms' counter block t >> 2 at its largest), from
+    a mid-episode state: every step inside the enclosures, the episode counters
+    continue from the state that was set, and one further step is rejected."""
+    import paper_2207_07736_amd as p
+    n, K, seed = 300, 48, 77
+    t_start = (1 << 32) - 1 - K
+    w = policy_weights(8, 0.3)
+    st, keep = device_policy(w, dtype)
+    sim = p.Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(seed)
+        state, _, _ = sim.get_state()
+        ep0 = np.random.default_rng(9).integers(0, 500, n).astype(np.uint32)
+        sim.set_state(state, ep0, t_start)
+        tr = p.Trajectory(K, n, p0=True, learner=True)
+        sim.step(16, tr.rows(0, 16), policy=st)
+        sim.step(K - 16, tr.rows(16, K - 16), policy=st)
+        torch.cuda.synchronize()
+        g = {key: getattr(tr, key).cpu().numpy() for key in ("obs", "action", "reward", "done", "policy_p0", "logp",
+                                                             "value")}
+        _, ep_end, t_end = sim.get_state()
+        assert t_end == (1 << 32) - 1
+        with pytest.raises(p.RlsimError) as e:
+            sim.step(1, policy=st)
+        assert e.value.code == p.RLSIM_EINVAL
+        del tr
+    finally:
+        sim.close()
+    del keep
+    assert np.array_equal(g["obs"][0], state)
+    assert (g["done"] & 2).any()
+    bad, first, stats = oracle.check_policy_rows(
+        oracle.make_params(**workloads.CARTPOLE), oracle.Policy(**w, bf16=(dtype == "bf16")), seed, 0, t_start,
+        g["obs"], g["action"], g["reward"], g["done"], g["policy_p0"], policy_bounds.errs(), logp=g["logp"],
+        value=g["value"], ep0=ep0)
+    assert bad == 0, (bad, first, stats)
+    if dtype == "f32":
+        assert stats["worst"] <= F32_P0_GATE, stats
+    # the episode counters: ep0 plus the steps since the last done (0 after it)
+    done_any = (g["done"] != 0)
+    last = np.where(done_any.any(axis=0), K - 1 - np.argmax(done_any[::-1], axis=0), -1)
+    want = np.where(last >= 0, K - 1 - last, ep0 + K).astype(np.uint32)
+    assert np.array_equal(ep_end, want)
