@@ -2,6 +2,8 @@
 //
 //  k_cartpole_fused<W>: one thread per environment; the cart-pole state and up
 //      to W padding words stay in registers for all K steps.
+//  k_cartpole_split: the same steps for D = 0 with a trajectory, with the
+//      stepping and the trajectory stores in separate waves of a workgroup.
 //  CartCore: the per-environment step loop every fused kernel shares (the
 //      wide-padding kernel in k_wide.hip.h and the policy kernel included).
 //  k_reset_cart, k_reset_pad: initial state and padding parameters.
@@ -111,8 +113,9 @@ struct CartCore {
     }
 
     // One step with the given action: record the row, Euler-step, terminate /
-    // truncate, auto-reset.  hook(act, reset) sees the action and whether the
-    // episode ended.  The row pointers are left for the caller to advance.
+    // truncate, auto-reset.  hook.record(obs, act, done byte) sees the row this
+    // step records and hook(act, reset) the action and whether the episode
+    // ended.  The row pointers are left for the caller to advance.
     template <class Hook>
     __device__ __forceinline__ void step_with(uint32_t act, Hook& hook)
     {
@@ -137,6 +140,7 @@ struct CartCore {
             *at(obs + 3 * plane, off4) = s.thd;
             *at(rew_row, off4) = 1.0f;
         }
+        hook.record(s, act, d);
         const bool reset = term || trunc;
         s.x = reset ? rs.x : nx.x;
         s.xd = reset ? rs.xd : nx.xd;
@@ -222,12 +226,14 @@ struct CartCore {
     }
 };
 
-// Sums the four episode counters over the workgroup and writes one row of the
-// block statistics (all threads of the block must call this).
+// Sums the four episode counters over a workgroup of kThreads threads and
+// writes one row of the block statistics (all threads of the block must call
+// this).
+template <uint32_t kThreads = kBlock>
 __device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t blk, uint32_t c0, uint32_t c1, uint32_t c2,
                                                   uint32_t c3)
 {
-    __shared__ uint32_t part[kBlock / 64][4];
+    __shared__ uint32_t part[kThreads / 64][4];
     const uint32_t v0 = wave_sum(c0), v1 = wave_sum(c1), v2 = wave_sum(c2), v3 = wave_sum(c3);
     const uint32_t wave = threadIdx.x / 64u, lane = threadIdx.x % 64u;
     if (lane == 0u) {
@@ -240,7 +246,7 @@ __device__ __forceinline__ void store_block_stats(uint32_t* stats, uint32_t blk,
     if (threadIdx.x < 4u) {
         uint32_t sum = 0u;
 #pragma unroll
-        for (int w = 0; w < kBlock / 64; ++w) sum += part[w][threadIdx.x];
+        for (int w = 0; w < (int)(kThreads / 64); ++w) sum += part[w][threadIdx.x];
         stats[(size_t)blk * 4u + threadIdx.x] = sum;
     }
 }
@@ -255,6 +261,7 @@ __device__ __forceinline__ float pad_update(float a, float s, float b, bool u)
 }
 
 struct NoPad {
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
     __device__ __forceinline__ void operator()(uint32_t, bool) {}
 };
 
@@ -262,6 +269,7 @@ struct NoPad {
 template <int W>
 struct RegisterPad {
     float s[W > 0 ? W : 1], a[W > 0 ? W : 1], b[W > 0 ? W : 1];
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
     __device__ __forceinline__ void operator()(uint32_t act, bool reset)
     {
 #pragma unroll
@@ -303,6 +311,123 @@ void k_cartpole_fused(StepArgs a)
         const uint32_t len_sum = env < a.n ? core.finished_length_sum(a.K) : 0u;
         store_block_stats(a.stats, blk, core.n_eps, len_sum, core.n_term, core.n_trunc);
     }
+}
+
+// ---------------------------------------------------------------------------
+// Warp-specialised stepping for D = 0 with a trajectory.
+// ---------------------------------------------------------------------------
+// A workgroup of 512 threads covers 256 environments.  Its first four waves
+// step them (one thread per environment, the CartCore loop with the state in
+// registers) and write each step's row into LDS instead of device memory; its
+// last four waves copy the rows from LDS to the trajectory, each step's seven
+// stores close together with no arithmetic between them.  The trajectory
+// stores then run at the rate of a store-only kernel, which they do not reach
+// when every wave interleaves them with the step's arithmetic.
+//
+// Rows are handed over in chunks of kHandSteps steps through two LDS buffers
+// and one workgroup barrier per chunk: between barriers c and c+1 the stepping
+// waves fill buffer (c+1) & 1 while the storing waves drain buffer c & 1, which
+// the steppers filled before barrier c.  Both sides pass ceil(K / kHandSteps)
+// barriers, then the one in the block statistics.  37 KB of LDS per workgroup
+// leaves room for four workgroups (eight waves per SIMD) per CU.
+constexpr uint32_t kHandSteps = 4;
+
+// CartCore hook of the stepping waves: records each step's row in the current
+// LDS buffer and passes a barrier after every kHandSteps steps.
+struct RowHandOver {
+    float (*obs)[kHandSteps][4][kBlock];     // [2 buffers][step][component][env]
+    uint16_t (*act_done)[kHandSteps][kBlock];  // action | done byte << 8
+    uint32_t col;                            // this thread's environment column
+    uint32_t i = 0u, buf = 0u;               // step within the chunk, buffer
+    __device__ __forceinline__ void record(const CartState& s, uint32_t act, uint32_t d)
+    {
+        obs[buf][i][0][col] = s.x;
+        obs[buf][i][1][col] = s.xd;
+        obs[buf][i][2][col] = s.th;
+        obs[buf][i][3][col] = s.thd;
+        act_done[buf][i][col] = (uint16_t)(act | (d << 8));
+    }
+    __device__ __forceinline__ void operator()(uint32_t, bool)
+    {
+        if (++i == kHandSteps) {
+            i = 0u;
+            buf ^= 1u;
+            __syncthreads();
+        }
+    }
+    // the barrier that hands over a last, partial chunk
+    __device__ __forceinline__ void flush()
+    {
+        if (i != 0u) __syncthreads();
+    }
+};
+
+// The storing waves' copy of one recorded step (row `row` of the call).
+__device__ __forceinline__ void store_handed_row(const StepArgs& a, size_t row, uint32_t off4, uint32_t off1,
+                                                 const float (*obs)[kBlock], const uint16_t* act_done, uint32_t col)
+{
+    const size_t plane = a.n;
+    const float x = obs[0][col], xd = obs[1][col], th = obs[2][col], thd = obs[3][col];
+    const uint32_t ad = act_done[col];
+    float* o = a.obs + row * 4 * plane;
+    *at(a.action + row * plane, off1) = (uint8_t)ad;
+    *at(a.done + row * plane, off1) = (uint8_t)(ad >> 8);
+    *at(o, off4) = x;
+    *at(o + plane, off4) = xd;
+    *at(o + 2 * plane, off4) = th;
+    *at(o + 3 * plane, off4) = thd;
+    *at(a.reward + row * plane, off4) = 1.0f;
+}
+
+template <bool STATS>
+__global__ __launch_bounds__(2 * kBlock) __attribute__((amdgpu_waves_per_eu(8)))
+void k_cartpole_split(StepArgs a)
+{
+    __shared__ float lds_obs[2][kHandSteps][4][kBlock];
+    __shared__ uint16_t lds_ad[2][kHandSteps][kBlock];
+    const uint32_t blk = xcd_block();
+    const uint32_t col = threadIdx.x % kBlock;
+    const uint32_t env = blk * kBlock + col;
+    const bool live = env < a.n;
+    uint32_t c0 = 0u, c1 = 0u, c2 = 0u, c3 = 0u;
+    if (threadIdx.x < kBlock) {
+        // stepping waves; threads past n step a zero state so that every wave
+        // passes the same barriers, and record nothing the storing side keeps
+        CartCore<false, STATS> core(a.p, env);
+        if (live) {
+            core.load(a);
+        } else {
+            core.s = CartState{0.0f, 0.0f, 0.0f, 0.0f};
+            core.ep = 0u;
+        }
+        RowHandOver h{lds_obs, lds_ad, col};
+        core.run(a.t0, a.K, h);
+        h.flush();
+        if (live) {
+            core.store(a);
+            c0 = core.n_eps;
+            c1 = core.finished_length_sum(a.K);
+            c2 = core.n_term;
+            c3 = core.n_trunc;
+        }
+    } else {
+        // storing waves: chunk c is complete after the c-th barrier
+        const uint32_t off4 = env * 4u, off1 = env;
+        const uint32_t n_chunks = a.K / kHandSteps + (a.K % kHandSteps != 0u ? 1u : 0u);
+        for (uint32_t c = 0; c < n_chunks; ++c) {
+            __syncthreads();
+            const uint32_t b = c & 1u, k0 = c * kHandSteps, m = min(kHandSteps, a.K - k0);
+            if (live && m == kHandSteps) {
+#pragma unroll
+                for (uint32_t i = 0; i < kHandSteps; ++i)
+                    store_handed_row(a, (size_t)k0 + i, off4, off1, lds_obs[b][i], lds_ad[b][i], col);
+            } else if (live) {
+                for (uint32_t i = 0; i < m; ++i)
+                    store_handed_row(a, (size_t)k0 + i, off4, off1, lds_obs[b][i], lds_ad[b][i], col);
+            }
+        }
+    }
+    if (STATS) store_block_stats<2 * kBlock>(a.stats, blk, c0, c1, c2, c3);
 }
 
 // ---------------------------------------------------------------------------

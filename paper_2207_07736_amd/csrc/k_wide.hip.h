@@ -26,6 +26,7 @@ struct BitRecorder {
     uint32_t col;        // threadIdx.x
     uint32_t k = 0u;     // step index within the round
     uint32_t ub = 0u, db = 0u;
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
     __device__ __forceinline__ void operator()(uint32_t act, bool reset)
     {
         const uint32_t bit = k & 31u;

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
-KERNEL = "void rlsim_dev::k_cartpole_fused<0, true, true>(rlsim_dev::StepArgs)"
+KERNEL = "void rlsim_dev::k_cartpole_split<true>(rlsim_dev::StepArgs)"
 COPY = "__amd_rocclr_copyBuffer"
 
 
@@ -30,7 +30,7 @@ def test_ingest_scales_by_the_copy_and_round_trips(tmp_path, monkeypatch):
     # the 1 GiB copy reads as half its bytes on FETCH_SIZE and exactly on WRITE_SIZE
     _csv(fetch, "FETCH_SIZE", [(KERNEL, 98.0), (KERNEL, 100.0), (KERNEL, 102.0), (COPY, 524288.0)])
     _csv(write, "WRITE_SIZE", [(KERNEL, 1000.0), (KERNEL, 1000.0), (KERNEL, 1010.0), (COPY, 1048576.0)])
-    bench.ingest_pmc(str(fetch), str(write), "wl", "void rlsim_dev::k_cartpole_fused<0")
+    bench.ingest_pmc(str(fetch), str(write), "wl", bench.HEADLINE_KERNEL_PREFIX)
     kv = bench._read_kv(str(out))
     assert float(kv["copy_fetch_scale"]) == 2.0 and float(kv["copy_write_scale"]) == 1.0
     # medians 100 and 1000 KiB: 100 * 1024 * 2 + 1000 * 1024 * 1
@@ -48,7 +48,7 @@ def test_ingest_needs_the_kernel_and_the_copy(tmp_path, monkeypatch):
     _csv(fetch, "FETCH_SIZE", [(KERNEL, 100.0)])
     _csv(write, "WRITE_SIZE", [(KERNEL, 1000.0)])
     with pytest.raises(SystemExit):
-        bench.ingest_pmc(str(fetch), str(write), "wl", "void rlsim_dev::k_cartpole_fused<0")
+        bench.ingest_pmc(str(fetch), str(write), "wl", bench.HEADLINE_KERNEL_PREFIX)
 
 
 def test_missing_summary_gives_no_traffic(tmp_path, monkeypatch):

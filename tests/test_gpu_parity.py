@@ -279,6 +279,42 @@ def test_last_steps_below_the_global_step_limit(D):
         sim.close()
 
 
+@pytest.mark.parametrize("n", [1, 63, 65, 257, 1000])
+def test_warp_specialised_chunk_tails_and_ragged_blocks(n):
+    """Trajectory calls of K >= 16 steps without padding words run the
+    warp-specialised kernel (rows handed from stepping to storing waves in
+    4-step chunks): K on and off the chunk size around the threshold, blocks
+    whose stepping waves are partly or wholly past n, with and without the
+    block statistics."""
+    sched = [15, 16, 17, 18, 19, 20, 33, 64]
+    T = sum(sched)
+    r = oracle_run(n, T, sched, seed=12)
+    for stats in (True, False):
+        g = gpu_run(n, T, sched, seed=12, stats=stats)
+        assert_bit_equal(g, r)
+        if stats:
+            _stats_equal(g["stats"], r["stats"])
+
+
+@pytest.mark.parametrize("overrides", [
+    dict(max_episode_steps=5),
+    dict(max_episode_steps=0, no_termination=1),
+    dict(max_episode_steps=3, x_threshold=0.01),
+    dict(max_episode_steps=1),
+    dict(force_mag=0.0, gravity=0.0),
+    dict(compute_factor=7),
+])
+def test_warp_specialised_edge_configs(overrides):
+    """The edge configurations and a compute factor through the
+    warp-specialised kernel (D = 0, K >= 16)."""
+    cfg = workloads.cartpole(**overrides)
+    n, T = 300, 120
+    g = gpu_run(n, T, [50, 70], seed=3, cfg=cfg)
+    r = oracle_run(n, T, [50, 70], seed=3, cfg=cfg)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
 @pytest.mark.parametrize("C", [2, 7, 64])
 def test_compute_factor_bit_exact(C):
     """The paper's compute factor: C Euler iterations of tau / C per step."""
