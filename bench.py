@@ -44,8 +44,8 @@ def traffic_file(workload: str) -> str:
 FUSED_KERNEL_SOURCES = ("device_common.hip.h", "k_cartpole.hip.h", "rlsim.hip")
 # the kernel a trajectory-recording launch of K >= 16 steps without padding
 # words runs (the headline launch), as rocprofv3 names it and as reported
-HEADLINE_KERNEL_PREFIX = "void rlsim_dev::k_cartpole_split<"
-HEADLINE_KERNEL = "k_cartpole_split<STATS>"
+HEADLINE_KERNEL_PREFIX = "void rlsim_dev::k_cartpole_split<0,"
+HEADLINE_KERNEL = "k_cartpole_split<0,STATS>"
 
 
 def kernel_source_digest() -> str:

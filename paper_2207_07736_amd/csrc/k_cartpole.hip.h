@@ -2,8 +2,9 @@
 //
 //  k_cartpole_fused<W>: one thread per environment; the cart-pole state and up
 //      to W padding words stay in registers for all K steps.
-//  k_cartpole_split: the same steps for D = 0 with a trajectory, with the
-//      stepping and the trajectory stores in separate waves of a workgroup.
+//  k_cartpole_split<W>: the same steps for up to W padding words with a
+//      trajectory, with the stepping and the trajectory stores in separate
+//      waves of a workgroup.
 //  CartCore: the per-environment step loop every fused kernel shares (the
 //      wide-padding kernel in k_wide.hip.h and the policy kernel included).
 //  k_reset_cart, k_reset_pad: initial state and padding parameters.
@@ -314,11 +315,12 @@ void k_cartpole_fused(StepArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Warp-specialised stepping for D = 0 with a trajectory.
+// Warp-specialised stepping for up to W padding words with a trajectory.
 // ---------------------------------------------------------------------------
 // A workgroup of 512 threads covers 256 environments.  Its first four waves
-// step them (one thread per environment, the CartCore loop with the state in
-// registers) and write each step's row into LDS instead of device memory; its
+// step them (one thread per environment, the CartCore loop with the state and
+// up to W padding words in registers) and write each step's row into LDS
+// instead of device memory; its
 // last four waves copy the rows from LDS to the trajectory, each step's seven
 // stores close together with no arithmetic between them.  The trajectory
 // stores then run at the rate of a store-only kernel, which they do not reach
@@ -379,7 +381,20 @@ __device__ __forceinline__ void store_handed_row(const StepArgs& a, size_t row, 
     *at(a.reward + row * plane, off4) = 1.0f;
 }
 
-template <bool STATS>
+// Both hooks of a stepping wave: the padding words' update and the hand-over.
+template <int W>
+struct PadHandOver {
+    RegisterPad<W>& pad;
+    RowHandOver& h;
+    __device__ __forceinline__ void record(const CartState& s, uint32_t act, uint32_t d) { h.record(s, act, d); }
+    __device__ __forceinline__ void operator()(uint32_t act, bool reset)
+    {
+        pad(act, reset);
+        h(act, reset);
+    }
+};
+
+template <int W, bool STATS>
 __global__ __launch_bounds__(2 * kBlock) __attribute__((amdgpu_waves_per_eu(8)))
 void k_cartpole_split(StepArgs a)
 {
@@ -401,9 +416,22 @@ void k_cartpole_split(StepArgs a)
             core.ep = 0u;
         }
         RowHandOver h{lds_obs, lds_ad, col};
-        core.run(a.t0, a.K, h);
+        RegisterPad<W> pad;
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            const bool on = live && (uint32_t)j < a.D;
+            const size_t q = (size_t)j * a.n + env;
+            pad.s[j] = on ? a.pad_s[q] : 0.0f;
+            pad.a[j] = on ? a.pad_a[q] : 0.0f;
+            pad.b[j] = on ? a.pad_b[q] : 0.0f;
+        }
+        PadHandOver<W> ph{pad, h};
+        core.run(a.t0, a.K, ph);
         h.flush();
         if (live) {
+#pragma unroll
+            for (int j = 0; j < W; ++j)
+                if ((uint32_t)j < a.D) a.pad_s[(size_t)j * a.n + env] = pad.s[j];
             core.store(a);
             c0 = core.n_eps;
             c1 = core.finished_length_sum(a.K);

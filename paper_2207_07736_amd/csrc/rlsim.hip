@@ -163,11 +163,14 @@ unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 // Largest padding count of the register-resident (one thread per env) kernel;
 // above it the two-phase wide kernel holds the words.
 constexpr uint32_t kMaxRegisterWords = 16u;
-// Fewest steps per call for which a trajectory-recording call without padding
-// words runs the warp-specialised kernel.  Below it the handover's pipeline
-// fill and drain cost more than the faster stores save (4,194,304 envs:
-// 26.5 against 23.5 us per step at K = 8, 20.1 against 21.1 at K = 16).
+// Fewest steps per call for which a trajectory-recording call runs the
+// warp-specialised kernel: without padding words, and with 1-4 padding words.
+// Below them the hand-over's pipeline fill and drain cost more than the faster
+// stores save (4,194,304 envs, D = 0: 26.5 against 23.5 us per step at K = 8,
+// 20.1 against 21.1 at K = 16; 262,144 envs, D = 4: 0.76 against 0.71 ms per
+// 512 steps at K = 16, 0.60 against 0.62 at K = 100).
 constexpr uint32_t kSplitMinSteps = 16u;
+constexpr uint32_t kSplitPadMinSteps = 64u;
 // Largest state: 2^24 padding words per environment (3 x 64 MiB of device
 // memory per environment), which keeps the wide kernel's 32-bit word indices
 // (row offsets, chunk counts) far from overflow.
@@ -179,7 +182,9 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
     const dim3 grid(grid_for(a.n)), block(kBlock);
     if (!wide) {
         if (a.D == 0u && REC && a.K >= kSplitMinSteps)
-            hipLaunchKernelGGL((k_cartpole_split<STATS>), grid, dim3(2 * kBlock), 0, s, a);
+            hipLaunchKernelGGL((k_cartpole_split<0, STATS>), grid, dim3(2 * kBlock), 0, s, a);
+        else if (a.D <= 4u && REC && a.K >= kSplitPadMinSteps)
+            hipLaunchKernelGGL((k_cartpole_split<4, STATS>), grid, dim3(2 * kBlock), 0, s, a);
         else if (a.D == 0u) hipLaunchKernelGGL((k_cartpole_fused<0, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);

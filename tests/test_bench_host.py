@@ -11,7 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 import bench  # noqa: E402
 
-KERNEL = "void rlsim_dev::k_cartpole_split<true>(rlsim_dev::StepArgs)"
+KERNEL = "void rlsim_dev::k_cartpole_split<0, true>(rlsim_dev::StepArgs)"
 COPY = "__amd_rocclr_copyBuffer"
 
 

@@ -296,6 +296,20 @@ def test_warp_specialised_chunk_tails_and_ragged_blocks(n):
             _stats_equal(g["stats"], r["stats"])
 
 
+@pytest.mark.parametrize("D", [1, 3, 4])
+@pytest.mark.parametrize("n", [1, 257, 1000])
+def test_warp_specialised_padding_words(D, n):
+    """Calls of K >= 64 steps with 1-4 padding words run the warp-specialised
+    kernel with the words in the stepping waves' registers; K = 63 does not.
+    Chunk tails, blocks past n and the padding state against the oracle."""
+    sched = [64, 65, 130, 63, 66]
+    T = sum(sched)
+    g = gpu_run(n, T, sched, D=D, seed=14)
+    r = oracle_run(n, T, sched, D=D, seed=14)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
 @pytest.mark.parametrize("overrides", [
     dict(max_episode_steps=5),
     dict(max_episode_steps=0, no_termination=1),
