@@ -16,6 +16,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -48,14 +49,23 @@ HEADLINE_KERNEL_PREFIX = "void rlsim_dev::k_cartpole_split<0,"
 HEADLINE_KERNEL = "k_cartpole_split<0,STATS>"
 
 
+def code_text(src: str) -> str:
+    """C++ source without its comments and with whitespace collapsed: what the
+    compiler sees, so that editing a comment leaves the digest alone."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def kernel_source_digest() -> str:
-    """Digest of the fused kernel's sources: a stored traffic measurement is used
-    only while the kernel it was taken on is unchanged."""
+    """Digest of the fused kernel's sources (code only, comments stripped): a
+    stored traffic measurement is used only while the kernel it was taken on is
+    unchanged."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2207_07736_amd", "csrc")
     for f in FUSED_KERNEL_SOURCES:
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(f.encode() + b"\0" + code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -55,3 +55,13 @@ def test_missing_summary_gives_no_traffic(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "traffic_file", lambda workload: str(tmp_path / "absent.txt"))
     assert bench.stored_traffic("wl") is None
 
+
+
+def test_kernel_digest_ignores_comments_but_not_code():
+    """The stored traffic stays valid across comment edits of the kernel sources
+    and is dropped when their code changes."""
+    src = "int f(int x) { // a comment\n  return x + 1; /* block\n comment */ }\n"
+    assert bench.code_text(src) == bench.code_text(src.replace("a comment", "another comment"))
+    assert bench.code_text(src) == bench.code_text(src.replace("  return", "\treturn"))
+    assert bench.code_text(src) != bench.code_text(src.replace("x + 1", "x + 2"))
+    assert "comment" not in bench.code_text(src)
