@@ -190,9 +190,11 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
         else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
         else hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
     } else {
-        // lanes per env x words per lane: 8 x 8 for up to 64 words (per-lane
-        // bits, 8 envs per wave); otherwise one env per wave with uniform bits
-        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<8, 8, REC, STATS>), grid, block, 0, s, a);
+        // lanes per env x words per lane: 8 x 4 for up to 32 words and 8 x 8 for
+        // up to 64 (per-lane bits, 8 envs per wave; a lane replays all W of its
+        // words, so W follows D); otherwise one env per wave with uniform bits
+        if (a.D <= 32u) hipLaunchKernelGGL((k_cartpole_wide<8, 4, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<8, 8, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<64, 4, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<64, 8, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<64, 16, REC, STATS>), grid, block, 0, s, a);

@@ -26,7 +26,7 @@ def _need_gpu():
 # D values cover every kernel shape: 8x8 lane groups (<= 64 words), one env per
 # wave with 4/8/16/32/64 words per lane, ragged rows (D not a multiple of 4 or
 # of the chunk) and several word chunks per env (D > 4096).
-@pytest.mark.parametrize("D", [17, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
+@pytest.mark.parametrize("D", [17, 32, 33, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
 def test_wide_padding_bit_exact(D):
     n = 260                                   # two stats blocks, ragged tail
     T = 140 if D > 1024 else 300
@@ -38,7 +38,7 @@ def test_wide_padding_bit_exact(D):
         assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("D", [64, 512])
+@pytest.mark.parametrize("D", [20, 64, 512])
 def test_wide_long_launch_crosses_chunks(D):
     """K larger than the 512-step LDS round: the padding words are carried over
     between rounds inside one launch."""
