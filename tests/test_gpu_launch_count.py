@@ -57,7 +57,7 @@ def _captured_node_types(hip, stream, fn):
         hip.hipGraphDestroy(g)
 
 
-@pytest.mark.parametrize("D", [0, 8, 40])
+@pytest.mark.parametrize("D", [0, 3, 8, 20, 40])
 def test_one_launch_per_step_call(hip, D):
     from paper_2207_07736_amd import Simulator, Trajectory
     s = torch.cuda.Stream()
