@@ -17,6 +17,12 @@ Training"; K steps per call as in "Simulator Kernel Fusion"):
 * ``Sim`` -- N environments with auto-reset, the random-action or MLP-policy
   loop, padding words (the paper's state-size factor S, Simulator Complexity)
   and per-256-env block statistics.
+* ``sincos`` -- the series sin/cos with a quadrant reduction for angles past
+  pi/4 (a swinging link, a pole with termination disabled).
+* ``chain_step`` / ``ChainSim`` -- the second, heavier simulator the paper's
+  Future Work calls for: a cart carrying a chain of N uniform rods, its
+  Lagrangian in mass-matrix form solved by elimination every step, with the
+  same random-action loop, auto-reset and statistics.
 
 Parity pins live in ``tests/test_oracle_*.py``.  Functions without an
 independent pin: none.
@@ -78,6 +84,15 @@ class _Policy(ctypes.Structure):
     ]
 
 
+CHAIN_MAX_LINKS = 8
+
+
+class ChainConsts(ctypes.Structure):
+    """Derived constants of the chain simulator (orc_chain_make_consts)."""
+    _fields_ = [("N", ctypes.c_uint32), ("m00", ctypes.c_float)] + [
+        (name, ctypes.c_float * (CHAIN_MAX_LINKS + 1)) for name in ("h", "g_diag", "lh", "gh")]
+
+
 _lib = None
 
 
@@ -101,6 +116,12 @@ def lib():
     L.orc_sin.restype = ctypes.c_float
     L.orc_cos.argtypes = [ctypes.c_float]
     L.orc_cos.restype = ctypes.c_float
+    L.orc_sin_series.argtypes = [ctypes.c_float]
+    L.orc_sin_series.restype = ctypes.c_float
+    L.orc_cos_series.argtypes = [ctypes.c_float]
+    L.orc_cos_series.restype = ctypes.c_float
+    L.orc_sincos.argtypes = [ctypes.c_float, f32p, f32p]
+    L.orc_sincos.restype = None
     L.orc_cartpole_step.argtypes = [ctypes.POINTER(Params), f32p, ctypes.c_int, f32p]
     L.orc_cartpole_step.restype = None
     L.orc_env_step.argtypes = [ctypes.POINTER(Params), f32p, ctypes.c_int, f32p]
@@ -143,8 +164,8 @@ def lib():
     L.orc_get_pad_params.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     L.orc_check_rows.argtypes = [ctypes.POINTER(Params), ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
                                  ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
-                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                 ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32)]
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32)]
     L.orc_check_rows.restype = ctypes.c_uint64
     L.orc_mlp_bounds.argtypes = [ctypes.POINTER(_Policy), ctypes.POINTER(ctypes.c_float), ctypes.POINTER(Errs),
                                  ctypes.POINTER(Bounds)]
@@ -153,11 +174,40 @@ def lib():
                                         ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                        ctypes.POINTER(Errs), ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(Errs), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint32),
                                         ctypes.POINTER(ctypes.c_uint32)]
     L.orc_check_policy_rows.restype = ctypes.c_uint64
     L.orc_get_pad_params.restype = None
+    # the chain simulator
+    L.orc_chain_make_consts.argtypes = [ctypes.POINTER(Params), ctypes.c_uint32, ctypes.POINTER(ChainConsts)]
+    L.orc_chain_make_consts.restype = ctypes.c_int
+    L.orc_chain_accel.argtypes = [ctypes.POINTER(ChainConsts), f32p, ctypes.c_float, f32p]
+    L.orc_chain_accel.restype = None
+    L.orc_chain_env_step.argtypes = [ctypes.POINTER(Params), ctypes.POINTER(ChainConsts), f32p, ctypes.c_int, f32p]
+    L.orc_chain_env_step.restype = None
+    L.orc_chain_terminated.argtypes = [ctypes.POINTER(Params), ctypes.c_uint32, f32p]
+    L.orc_chain_terminated.restype = ctypes.c_int
+    L.orc_chain_reset_draw.argtypes = [ctypes.POINTER(Params), ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.c_uint32, f32p]
+    L.orc_chain_reset_draw.restype = None
+    L.orc_chain_create.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(Params)]
+    L.orc_chain_create.restype = ctypes.c_void_p
+    L.orc_chain_destroy.argtypes = [ctypes.c_void_p]
+    L.orc_chain_destroy.restype = None
+    L.orc_chain_reset.argtypes = [ctypes.c_void_p, ctypes.c_uint64]
+    L.orc_chain_reset.restype = None
+    L.orc_chain_step.argtypes = [ctypes.c_void_p, ctypes.c_uint32] + [ctypes.c_void_p] * 5
+    L.orc_chain_step.restype = ctypes.c_int
+    L.orc_chain_get_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint64)]
+    L.orc_chain_get_state.restype = None
+    L.orc_chain_set_state.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+    L.orc_chain_set_state.restype = ctypes.c_int
+    L.orc_chain_check_rows.argtypes = [ctypes.POINTER(Params), ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32] + [ctypes.c_void_p] * 7 + [
+                                       ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32)]
+    L.orc_chain_check_rows.restype = ctypes.c_uint64
     _lib = L
     return L
 
@@ -204,6 +254,22 @@ def sin_poly(th: float) -> np.float32:
 
 def cos_poly(th: float) -> np.float32:
     return np.float32(lib().orc_cos(float(np.float32(th))))
+
+
+def sin_series(th: float) -> np.float32:
+    return np.float32(lib().orc_sin_series(float(np.float32(th))))
+
+
+def cos_series(th: float) -> np.float32:
+    return np.float32(lib().orc_cos_series(float(np.float32(th))))
+
+
+def sincos(th: float):
+    """(sin, cos) of an fp32 angle: the series on |th| <= fp32(pi/4), quadrant
+    reduction outside it."""
+    s, c = ctypes.c_float(), ctypes.c_float()
+    lib().orc_sincos(float(np.float32(th)), ctypes.byref(s), ctypes.byref(c))
+    return np.float32(s.value), np.float32(c.value)
 
 
 def cartpole_step(params: Params, state, action: int) -> np.ndarray:
@@ -383,43 +449,178 @@ class Sim:
         return a, b
 
 
-def check_rows(params: Params, seed: int, env0: int, t0: int, obs, action, reward, done, ep0=None):
+def check_rows(params: Params, seed: int, env0: int, t0: int, obs, action, reward, done, ep0=None,
+               final_state=None, final_ep=None):
     """Teacher-forced check of recorded random-action rows ([K][4][n] obs,
-    [K][n] action / reward / done for envs env0 ..): returns (number of
-    mismatching env-steps, (k, i) of the first or None)."""
+    [K][n] action / reward / done for envs env0 ..).  ep0 None: every episode
+    began at t0, so row 0 must be the reset draw for t0.  final_state ([4][n])
+    and final_ep ([n]), optional, must be the state after the last row.
+    Returns (number of mismatching env-steps, (k, i) of the first or None)."""
     obs = np.ascontiguousarray(obs, dtype=np.float32)
     action = np.ascontiguousarray(action, dtype=np.uint8)
     reward = np.ascontiguousarray(reward, dtype=np.float32)
     done = np.ascontiguousarray(done, dtype=np.uint8)
     K, four, n = obs.shape
     assert four == 4 and action.shape == reward.shape == done.shape == (K, n)
-    e = None if ep0 is None else np.ascontiguousarray(ep0, dtype=np.uint32)
+    c = lambda x, dt: None if x is None else np.ascontiguousarray(x, dtype=dt)  # noqa: E731
+    e, fs, fe = c(ep0, np.uint32), c(final_state, np.float32), c(final_ep, np.uint32)
+    assert fs is None or fs.shape == (4, n)
+    assert fe is None or fe.shape == (n,)
+    ptr = lambda x: None if x is None else x.ctypes.data  # noqa: E731
     bk, bi = ctypes.c_uint32(0), ctypes.c_uint32(0)
     bad = lib().orc_check_rows(ctypes.byref(params), int(seed), int(env0), int(n), int(t0), int(K),
-                               None if e is None else e.ctypes.data, obs.ctypes.data, action.ctypes.data,
-                               reward.ctypes.data, done.ctypes.data, ctypes.byref(bk), ctypes.byref(bi))
+                               ptr(e), obs.ctypes.data, action.ctypes.data, reward.ctypes.data, done.ctypes.data,
+                               ptr(fs), ptr(fe), ctypes.byref(bk), ctypes.byref(bi))
     return int(bad), ((int(bk.value), int(bi.value)) if bad else None)
 
 
 def check_policy_rows(params: Params, policy: "Policy", seed: int, env0: int, t0: int, obs, action, reward, done,
-                      p0, errs: "Errs", logp=None, value=None, ep0=None):
+                      p0, errs: "Errs", logp=None, value=None, ep0=None, final_state=None, final_ep=None,
+                      dp0_out=None):
     """Teacher-forced check of recorded policy rows against the enclosures of
     orc_mlp_bounds under errs.  Returns (failing env-steps, first failure (k, i)
     or None, stats) with stats = dict(worst: max |p0 - oracle p0|, max_width and
     mean_width of the p0 enclosures, exempt: actions that differ from the
-    oracle's own choice, necessarily with u inside the enclosure)."""
+    oracle's own choice, necessarily with u inside the enclosure).  ep0,
+    final_state and final_ep as for check_rows; dp0_out, a float32 [K][n]
+    array, receives |p0 - oracle p0| of every env-step."""
     c = lambda x, dt: None if x is None else np.ascontiguousarray(x, dtype=dt)  # noqa: E731
     obs, action, reward, done = c(obs, np.float32), c(action, np.uint8), c(reward, np.float32), c(done, np.uint8)
     p0, logp, value, ep0 = c(p0, np.float32), c(logp, np.float32), c(value, np.float32), c(ep0, np.uint32)
+    fs, fe = c(final_state, np.float32), c(final_ep, np.uint32)
     K, four, n = obs.shape
     assert four == 4 and action.shape == reward.shape == done.shape == p0.shape == (K, n)
+    if dp0_out is not None:
+        assert dp0_out.dtype == np.float32 and dp0_out.shape == (K, n) and dp0_out.flags.c_contiguous
     ptr = lambda x: None if x is None else x.ctypes.data  # noqa: E731
     st = (ctypes.c_double * 3)()
     ex = ctypes.c_uint64(0)
     bk, bi = ctypes.c_uint32(0), ctypes.c_uint32(0)
     bad = lib().orc_check_policy_rows(ctypes.byref(params), ctypes.byref(policy.struct), int(seed), int(env0), int(n),
                                       int(t0), int(K), ptr(ep0), ptr(obs), ptr(action), ptr(reward), ptr(done),
-                                      ptr(p0), ptr(logp), ptr(value), ctypes.byref(errs), st, ctypes.byref(ex),
+                                      ptr(p0), ptr(logp), ptr(value), ctypes.byref(errs), ptr(fs), ptr(fe),
+                                      ptr(dp0_out), st, ctypes.byref(ex),
                                       ctypes.byref(bk), ctypes.byref(bi))
     stats = dict(worst=st[0], max_width=st[1], mean_width=st[2] / max(1, K * n), exempt=int(ex.value))
     return int(bad), ((int(bk.value), int(bi.value)) if bad else None), stats
+
+
+# ---------------------------------------------------------------------------
+# The chain simulator: a cart carrying N identical uniform rods.
+# ---------------------------------------------------------------------------
+def chain_consts(params: Params, n_links: int) -> ChainConsts:
+    k = ChainConsts()
+    if lib().orc_chain_make_consts(ctypes.byref(params), int(n_links), ctypes.byref(k)) != 0:
+        raise ValueError(f"n_links must be in [1, {CHAIN_MAX_LINKS}]")
+    return k
+
+
+def chain_accel(params: Params, n_links: int, state, force: float) -> np.ndarray:
+    """Accelerations (xdd, phidd_1..N) of a chain state (x, xd, phi_1, phid_1, ...)."""
+    k = chain_consts(params, n_links)
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    assert s.shape == (2 * (n_links + 1),)
+    out = np.zeros(n_links + 1, dtype=np.float32)
+    P = ctypes.POINTER(ctypes.c_float)
+    lib().orc_chain_accel(ctypes.byref(k), s.ctypes.data_as(P), float(force), out.ctypes.data_as(P))
+    return out
+
+
+def chain_step(params: Params, n_links: int, state, action: int) -> np.ndarray:
+    """One simulation step of the chain (compute_factor Euler iterations)."""
+    k = chain_consts(params, n_links)
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    assert s.shape == (2 * (n_links + 1),)
+    out = np.zeros_like(s)
+    P = ctypes.POINTER(ctypes.c_float)
+    lib().orc_chain_env_step(ctypes.byref(params), ctypes.byref(k), s.ctypes.data_as(P), int(action),
+                             out.ctypes.data_as(P))
+    return out
+
+
+def chain_terminated(params: Params, n_links: int, state) -> bool:
+    s = np.ascontiguousarray(state, dtype=np.float32)
+    return bool(lib().orc_chain_terminated(ctypes.byref(params), int(n_links),
+                                           s.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+
+
+def chain_reset_draw(params: Params, n_links: int, seed: int, env: int, t: int) -> np.ndarray:
+    out = np.zeros(2 * (n_links + 1), dtype=np.float32)
+    lib().orc_chain_reset_draw(ctypes.byref(params), int(n_links), int(seed), int(env), int(t),
+                               out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
+    return out
+
+
+class ChainSim:
+    """A slice of chain environments with global ids env0 .. env0+n-1."""
+
+    def __init__(self, n_envs: int, n_links: int, params: Params, env0: int = 0):
+        self.n, self.N, self.env0 = int(n_envs), int(n_links), int(env0)
+        self.S = 2 * (self.N + 1)
+        self.params = params
+        self._h = lib().orc_chain_create(self.n, self.env0, self.N, ctypes.byref(params))
+        if not self._h:
+            raise ValueError("orc_chain_create failed (bad n_links or compute_factor, or out of memory)")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            lib().orc_chain_destroy(h)
+            self._h = None
+
+    @property
+    def n_blocks(self) -> int:
+        return (self.env0 + self.n - 1) // 256 - self.env0 // 256 + 1
+
+    def reset(self, seed: int) -> None:
+        lib().orc_chain_reset(self._h, int(seed))
+
+    def step(self, K: int, record: bool = True, stats: bool = True):
+        n, S = self.n, self.S
+        out = {}
+        if record:
+            out["obs"] = np.empty((K, S, n), dtype=np.float32)
+            out["action"] = np.empty((K, n), dtype=np.uint8)
+            out["reward"] = np.empty((K, n), dtype=np.float32)
+            out["done"] = np.empty((K, n), dtype=np.uint8)
+        if stats:
+            out["stats"] = np.empty((self.n_blocks, 4), dtype=np.uint32)
+        ptr = lambda key: out[key].ctypes.data if key in out else None  # noqa: E731
+        rc = lib().orc_chain_step(self._h, int(K), ptr("obs"), ptr("action"), ptr("reward"), ptr("done"), ptr("stats"))
+        if rc != 0:
+            raise RuntimeError(f"orc_chain_step failed ({rc})")
+        return out
+
+    def get_state(self):
+        st = np.empty((self.S, self.n), dtype=np.float32)
+        ep = np.empty(self.n, dtype=np.uint32)
+        t = ctypes.c_uint64()
+        lib().orc_chain_get_state(self._h, st.ctypes.data, ep.ctypes.data, ctypes.byref(t))
+        return st, ep, int(t.value)
+
+    def set_state(self, state, ep, t: int) -> None:
+        st = np.ascontiguousarray(state, dtype=np.float32)
+        e = np.ascontiguousarray(ep, dtype=np.uint32)
+        if st.shape != (self.S, self.n) or e.shape != (self.n,):
+            raise ValueError("state shape mismatch")
+        rc = lib().orc_chain_set_state(self._h, st.ctypes.data, e.ctypes.data, int(t))
+        if rc != 0:
+            raise RuntimeError(f"orc_chain_set_state failed ({rc})")
+
+
+def chain_check_rows(params: Params, n_links: int, seed: int, env0: int, t0: int, obs, action, reward, done,
+                     ep0=None, final_state=None, final_ep=None):
+    """check_rows for the chain simulator ([K][2N+2][n] obs)."""
+    c = lambda x, dt: None if x is None else np.ascontiguousarray(x, dtype=dt)  # noqa: E731
+    obs, action, reward, done = c(obs, np.float32), c(action, np.uint8), c(reward, np.float32), c(done, np.uint8)
+    e, fs, fe = c(ep0, np.uint32), c(final_state, np.float32), c(final_ep, np.uint32)
+    K, S, n = obs.shape
+    assert S == 2 * (n_links + 1) and action.shape == reward.shape == done.shape == (K, n)
+    assert fs is None or fs.shape == (S, n)
+    assert fe is None or fe.shape == (n,)
+    ptr = lambda x: None if x is None else x.ctypes.data  # noqa: E731
+    bk, bi = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    bad = lib().orc_chain_check_rows(ctypes.byref(params), int(n_links), int(seed), int(env0), int(n), int(t0), int(K),
+                                     ptr(e), ptr(obs), ptr(action), ptr(reward), ptr(done), ptr(fs), ptr(fe),
+                                     ctypes.byref(bk), ctypes.byref(bi))
+    return int(bad), ((int(bk.value), int(bi.value)) if bad else None)

@@ -26,7 +26,15 @@
  *
  * Test helpers built on these definitions: orc_mlp_bounds (after the policy),
  * the interval enclosure of a device evaluation of the policy that serves as
- * its tolerance, and the teacher-forced row checkers (at the end).
+ * its tolerance, and the teacher-forced row checkers.
+ *
+ * The second simulator, a cart carrying a chain of N uniform rods (the
+ * heavier multi-body kind the paper's Future Work points to), closes the
+ * file: its Lagrangian in mass-matrix form, solved by elimination every
+ * step, with the same loop, RNG contract and checker.  Its pins: an
+ * independent 50-digit assembly of the equations of motion from the links'
+ * geometry, first-order energy and momentum drift, small-angle
+ * linearisation, and the one-link case against the cart-pole.
  */
 #include <math.h>
 #include <stdint.h>
@@ -96,11 +104,18 @@ typedef struct {
 } orc_params;
 
 /* ------------------------------------------------------------------------ */
-/* Truncated Maclaurin series for sin and cos, Horner form with fmaf.        */
-/* Used for |theta| <= 12 degrees (every pre-step state of a live episode),  */
-/* where the truncation error is below 1e-15.                                */
+/* sin and cos: a truncated Maclaurin series (degree 9 / 8, Horner form with  */
+/* fmaf) on |theta| <= fp32(pi/4), the domain of every pre-step angle of a    */
+/* live cart-pole episode.  Larger angles (a swinging chain link, a pole with */
+/* termination disabled) are first reduced by quadrants: k = the integer      */
+/* nearest theta * 2/pi (fp32 product, ties to even), r = theta - k pi/2 with */
+/* pi/2 split into a high fp32 part (r1 = theta - k * hi is exact: both terms */
+/* are multiples of 2^-24 and |r1| < 2) and a low part, then the quadrant     */
+/* k mod 4 (formed exactly in fp32) picks and signs the series values:        */
+/* sin(r + k pi/2) = sin r, cos r, -sin r, -cos r for k = 0, 1, 2, 3 mod 4.   */
+/* A non-finite theta gives NaN.                                              */
 /* ------------------------------------------------------------------------ */
-float orc_sin(float th)
+float orc_sin_series(float th)
 {
     const float s3 = (float)(-1.0 / 6.0);
     const float s5 = (float)(1.0 / 120.0);
@@ -114,7 +129,7 @@ float orc_sin(float th)
     return fmaf(th3, q, th);          /* th + th^3 (s3 + s5 z + s7 z^2 + s9 z^3) */
 }
 
-float orc_cos(float th)
+float orc_cos_series(float th)
 {
     const float c2 = -0.5f;
     const float c4 = (float)(1.0 / 24.0);
@@ -125,6 +140,51 @@ float orc_cos(float th)
     q = fmaf(q, z, c4);
     q = fmaf(q, z, c2);
     return fmaf(z, q, 1.0f);          /* 1 + z (c2 + c4 z + c6 z^2 + c8 z^3) */
+}
+
+void orc_sincos(float th, float* s, float* c)
+{
+    const float quarter_pi = (float)(3.14159265358979323846 / 4.0);        /* 0x3F490FDB */
+    const float two_over_pi = (float)(2.0 / 3.14159265358979323846);      /* 0x3F22F983 */
+    const float half_pi_hi = (float)(3.14159265358979323846 / 2.0);       /* 0x3FC90FDB */
+    const float half_pi_lo = -4.371138828673793e-08f;                     /* 0xB33BBD2E = fp32(pi/2 - hi) */
+    if (fabsf(th) <= quarter_pi) {
+        *s = orc_sin_series(th);
+        *c = orc_cos_series(th);
+        return;
+    }
+    float k = rintf(th * two_over_pi);
+    float r = fmaf(-k, half_pi_hi, th);
+    r = fmaf(-k, half_pi_lo, r);
+    float quadrant = k - 4.0f * floorf(k * 0.25f);      /* k mod 4, exact; NaN for non-finite theta */
+    float sr = orc_sin_series(r), cr = orc_cos_series(r);
+    if (quadrant == 1.0f) {
+        *s = cr;
+        *c = -sr;
+    } else if (quadrant == 2.0f) {
+        *s = -sr;
+        *c = -cr;
+    } else if (quadrant == 3.0f) {
+        *s = -cr;
+        *c = sr;
+    } else {
+        *s = sr;
+        *c = cr;
+    }
+}
+
+float orc_sin(float th)
+{
+    float s, c;
+    orc_sincos(th, &s, &c);
+    return s;
+}
+
+float orc_cos(float th)
+{
+    float s, c;
+    orc_sincos(th, &s, &c);
+    return c;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -149,8 +209,8 @@ void orc_cartpole_step(const orc_params* p, const float in[4], int action, float
     float x = in[0], xd = in[1], th = in[2], thd = in[3];
     float force = action ? p->force_mag : -p->force_mag;
 
-    float sin_th = orc_sin(th);
-    float cos_th = orc_cos(th);
+    float sin_th, cos_th;
+    orc_sincos(th, &sin_th, &cos_th);
 
     float thd2 = thd * thd;
     float ml_thd2 = pole_ml * thd2;
@@ -658,18 +718,23 @@ void orc_get_pad_params(const orc_sim* sim, float* a, float* b)
 /* comparison rule that every recorded step follows from the one before it).  */
 /* Rows k = 0..K-1 hold global steps t0 + k of environments env0 .. env0+n-1, */
 /* laid out [K][4][n] (obs) and [K][n] (action, reward, done); ep0[i] is the   */
-/* episode's step count at t0 (NULL: 0 for every env, as after a reset).  For */
+/* episode's step count at t0.  ep0 == NULL means every episode began at t0   */
+/* (as after a reset), so row 0 must also be the reset draw for step t0.  For */
 /* every env-step it recomputes, from the recorded obs and nothing else:      */
 /*   the random action bit of (seed, env, t), reward 1,                       */
 /*   next = the simulation step of (obs_t, action),                           */
 /*   done = terminated(next) | truncated << 1 (episode length from ep0),      */
 /*   obs_{t+1} (row k+1) = the reset draw for step t+1 if done, else next,    */
-/* bit for bit.  Returns the number of mismatching env-steps and, if any, the */
-/* row and env index of the first in *bad_k, *bad_i.                         */
+/* bit for bit.  final_state ([4][n]) and final_ep ([n]), each optional, are  */
+/* the state and episode counters after the last row: they must equal the    */
+/* last step's successor and episode length (mismatches count at row K-1).    */
+/* Returns the number of mismatching env-steps and, if any, the row and env   */
+/* index of the first in *bad_k, *bad_i.                                      */
 /* ------------------------------------------------------------------------ */
 uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint32_t n, uint32_t t0, uint32_t K,
                         const uint32_t* ep0, const float* obs, const uint8_t* act, const float* rew,
-                        const uint8_t* done, uint32_t* bad_k, uint32_t* bad_i)
+                        const uint8_t* done, const float* final_state, const uint32_t* final_ep,
+                        uint32_t* bad_k, uint32_t* bad_i)
 {
     uint64_t bad = 0;
     for (uint32_t i = 0; i < n; ++i) {
@@ -679,14 +744,20 @@ uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint3
             uint32_t t = t0 + k;
             float cur[4], nxt[4];
             for (int c = 0; c < 4; ++c) cur[c] = obs[((size_t)k * 4 + c) * n + i];
+            int ok = 1;
+            if (k == 0 && !ep0) {
+                float start[4];
+                orc_reset_draw(p, seed, env, t0, start);
+                if (memcmp(start, cur, sizeof(start)) != 0) ok = 0;
+            }
             int a = orc_action_bit(seed, env, t);
             orc_env_step(p, cur, a, nxt);
             uint32_t len = ep + 1u;
             int term = orc_terminated(p, nxt);
             int trunc = (p->max_episode_steps != 0u) && (len >= p->max_episode_steps);
             uint8_t d = (uint8_t)(term | (trunc << 1));
-            int ok = act[(size_t)k * n + i] == (uint8_t)a && rew[(size_t)k * n + i] == 1.0f &&
-                     done[(size_t)k * n + i] == d;
+            if (act[(size_t)k * n + i] != (uint8_t)a || rew[(size_t)k * n + i] != 1.0f || done[(size_t)k * n + i] != d)
+                ok = 0;
             if (d) {
                 orc_reset_draw(p, seed, env, t + 1u, nxt);
                 ep = 0u;
@@ -698,6 +769,13 @@ uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint3
                     float g = obs[((size_t)(k + 1) * 4 + c) * n + i];
                     if (memcmp(&g, &nxt[c], sizeof(float)) != 0) ok = 0;
                 }
+            }
+            if (ok && k + 1 == K) {
+                for (int c = 0; c < 4 && final_state; ++c) {
+                    float g = final_state[(size_t)c * n + i];
+                    if (memcmp(&g, &nxt[c], sizeof(float)) != 0) ok = 0;
+                }
+                if (final_ep && final_ep[i] != ep) ok = 0;
             }
             if (!ok) {
                 if (bad == 0 && bad_k && bad_i) {
@@ -722,8 +800,12 @@ uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint3
 /*   reward 1, the done byte, and the next row (reset draw after an episode   */
 /*   end) follow from the simulation step of (obs, recorded action), bit for  */
 /*   bit.                                                                    */
+/* ep0 == NULL (episodes begin at t0) also checks row 0 against the reset    */
+/* draw, and final_state / final_ep (optional) the state after the last row,  */
+/* as orc_check_rows does.                                                    */
 /* An action that differs from the oracle's own choice (u < p0) can only be   */
 /* one whose u lies inside the p0 enclosure; these are counted in *exempt.    */
+/* dp0_out ([K][n], may be NULL) receives |p0g - p0| of every env-step.        */
 /* stats (may be NULL): [0] max |p0g - p0|, [1] max p0 enclosure width,        */
 /* [2] sum of p0 enclosure widths.  Returns the number of failing env-steps;  */
 /* *bad_k, *bad_i the first failure.                                          */
@@ -731,7 +813,8 @@ uint64_t orc_check_rows(const orc_params* p, uint64_t seed, uint32_t env0, uint3
 uint64_t orc_check_policy_rows(const orc_params* p, const orc_policy* pol, uint64_t seed, uint32_t env0, uint32_t n,
                                uint32_t t0, uint32_t K, const uint32_t* ep0, const float* obs, const uint8_t* act,
                                const float* rew, const uint8_t* done, const float* p0g, const float* logp,
-                               const float* value, const orc_errs* errs, double stats[3], uint64_t* exempt,
+                               const float* value, const orc_errs* errs, const float* final_state,
+                               const uint32_t* final_ep, float* dp0_out, double stats[3], uint64_t* exempt,
                                uint32_t* bad_k, uint32_t* bad_i)
 {
     uint64_t bad = 0, ex = 0;
@@ -766,9 +849,15 @@ uint64_t orc_check_policy_rows(const orc_params* p, const orc_policy* pol, uint6
             orc_mlp_bounds(&rp, cur, errs, &bd);
             double g = (double)p0g[q];
             if (fabs(g - p0) > worst) worst = fabs(g - p0);
+            if (dp0_out) dp0_out[q] = (float)fabs(g - p0);
             if (bd.p0_hi - bd.p0_lo > wmax) wmax = bd.p0_hi - bd.p0_lo;
             wsum += bd.p0_hi - bd.p0_lo;
             int ok = (a == (u < p0g[q] ? 0 : 1)) && g >= bd.p0_lo && g <= bd.p0_hi;
+            if (k == 0 && !ep0) {
+                float start[4];
+                orc_reset_draw(p, seed, env, t0, start);
+                if (memcmp(start, cur, sizeof(start)) != 0) ok = 0;
+            }
             if (a != (((double)u < p0) ? 0 : 1)) ++ex;
             if (logp) {
                 double l = (double)logp[q];
@@ -793,6 +882,13 @@ uint64_t orc_check_policy_rows(const orc_params* p, const orc_policy* pol, uint6
                     if (memcmp(&gnext, &nxt[c], sizeof(float)) != 0) ok = 0;
                 }
             }
+            if (ok && k + 1 == K) {
+                for (int c = 0; c < 4 && final_state; ++c) {
+                    float gnext = final_state[(size_t)c * n + i];
+                    if (memcmp(&gnext, &nxt[c], sizeof(float)) != 0) ok = 0;
+                }
+                if (final_ep && final_ep[i] != ep) ok = 0;
+            }
             if (!ok) {
                 if (bad == 0 && bad_k && bad_i) {
                     *bad_k = k;
@@ -808,5 +904,378 @@ uint64_t orc_check_policy_rows(const orc_params* p, const orc_policy* pol, uint6
         stats[2] = wsum;
     }
     if (exempt) *exempt = ex;
+    return bad;
+}
+
+/* ======================================================================== */
+/* Second simulator: a cart carrying a chain of N identical uniform rods.    */
+/* The paper's Future Work points to heavier, multi-body simulators (its      */
+/* Related Work names rigid-body engines); it gives no model, so this one is  */
+/* derived here from its Lagrangian.                                          */
+/*                                                                            */
+/* Cart of mass mc on a frictionless track; links k = 1..N, each a uniform    */
+/* rod of mass m and length L = 2 l, joined end to end, link 1 hinged on the  */
+/* cart.  Generalised coordinates q = (x, phi_1, ..., phi_N), phi_k the angle */
+/* of link k from the upward vertical (a link leaning towards +x has          */
+/* positive phi).  With mu_k = (N - k) m the mass beyond link k:              */
+/*   h_k = L (m/2 + mu_k)      (cart coupling / first moment of link k)       */
+/*   G_kk = L^2 (m/3 + mu_k),  G_jk = L h_k for j < k   (link coupling)       */
+/* the kinetic energy is                                                      */
+/*   T = 1/2 (mc + N m) xd^2 + sum_k h_k cos(phi_k) xd phid_k                 */
+/*       + 1/2 sum_jk G_jk cos(phi_j - phi_k) phid_j phid_k                   */
+/* and the potential V = g sum_k h_k cos(phi_k), so Lagrange's equations are  */
+/* M(q) qdd = f(q, qd) with the symmetric mass matrix                         */
+/*   M_00 = mc + N m,  M_0k = h_k cos(phi_k),  M_jk = G_jk cos(phi_j - phi_k) */
+/* and the forces                                                             */
+/*   f_0 = F + sum_k h_k sin(phi_k) phid_k^2                                  */
+/*   f_j = g h_j sin(phi_j) - sum_{k != j} G_jk sin(phi_j - phi_k) phid_k^2.  */
+/* N = 1 is the cart-pole above (h = m l, G = 4/3 m l^2).                     */
+/*                                                                            */
+/* The fp32 evaluation, in this order (the GPU kernel does the same):         */
+/*  - constants from (mc, m, l, g), once, one operation each: L = 2 l,        */
+/*    mu_k = (N - k) * m, h_k = L * (0.5 m + mu_k), G_kk = (L * L) *          */
+/*    (m / 3 + mu_k), Lh_k = L * h_k, gh_k = g * h_k, M_00 = mc + N * m;      */
+/*  - (s_k, c_k) = sincos(phi_k) (the full-range form above), w_k = phid_k^2; */
+/*  - cos(phi_j - phi_k) = fma(c_j, c_k, s_j s_k) and                         */
+/*    sin(phi_j - phi_k) = fma(s_j, c_k, -(c_j s_k)) for each pair j < k;     */
+/*  - f_0 = F, then f_0 = fma(h_k s_k, w_k, f_0) for k = 1..N; f_j = gh_j s_j, */
+/*    then for each pair j < k in lexicographic order, P = Lh_k sin(phi_j -   */
+/*    phi_k): f_j = fma(-P, w_k, f_j), f_k = fma(P, w_j, f_k);                */
+/*  - Gaussian elimination without pivoting (M is positive definite) on the  */
+/*    upper triangle: for pivot p, inv_p = 1 / A_pp (IEEE division), for      */
+/*    i > p: l = A_pi inv_p, A_ij = fma(-l, A_pj, A_ij) for j >= i,           */
+/*    f_i = fma(-l, f_p, f_i); then back substitution                         */
+/*    qdd_i = (f_i - sum_{j > i} A_ij qdd_j) inv_i, the sum as fmas from      */
+/*    j = i + 1 upwards;                                                      */
+/*  - explicit Euler: positions advance with the old velocities.             */
+/* ======================================================================== */
+#define ORC_CHAIN_MAX_LINKS 8
+
+typedef struct {
+    uint32_t N;
+    float m00;                                    /* mc + N m */
+    float h[ORC_CHAIN_MAX_LINKS + 1];             /* [1..N] */
+    float g_diag[ORC_CHAIN_MAX_LINKS + 1];        /* G_kk */
+    float lh[ORC_CHAIN_MAX_LINKS + 1];            /* L h_k = G_jk for j < k */
+    float gh[ORC_CHAIN_MAX_LINKS + 1];            /* g h_k */
+} orc_chain_consts;
+
+int orc_chain_make_consts(const orc_params* p, uint32_t N, orc_chain_consts* k)
+{
+    if (N < 1 || N > ORC_CHAIN_MAX_LINKS) return -1;
+    memset(k, 0, sizeof(*k));
+    k->N = N;
+    float m = p->masspole;
+    float L = 2.0f * p->half_length;
+    float LL = L * L;
+    float half_m = 0.5f * m;
+    float third_m = m / 3.0f;
+    for (uint32_t j = 1; j <= N; ++j) {
+        float mu = (float)(N - j) * m;
+        float hm = half_m + mu;
+        k->h[j] = L * hm;
+        float gm = third_m + mu;
+        k->g_diag[j] = LL * gm;
+        k->lh[j] = L * k->h[j];
+        k->gh[j] = p->gravity * k->h[j];
+    }
+    float nm = (float)N * m;
+    k->m00 = p->masscart + nm;
+    return 0;
+}
+
+/* Accelerations qdd = (xdd, phidd_1..N) of the state (x, xd, phi_1, phid_1, ...) */
+/* under the cart force F. */
+void orc_chain_accel(const orc_chain_consts* k, const float* st, float force, float* qdd)
+{
+    uint32_t N = k->N, S = N + 1;
+    float s[ORC_CHAIN_MAX_LINKS + 1], c[ORC_CHAIN_MAX_LINKS + 1], w[ORC_CHAIN_MAX_LINKS + 1];
+    float A[ORC_CHAIN_MAX_LINKS + 1][ORC_CHAIN_MAX_LINKS + 1], f[ORC_CHAIN_MAX_LINKS + 1];
+    float inv[ORC_CHAIN_MAX_LINKS + 1];
+    for (uint32_t j = 1; j <= N; ++j) {
+        float phi = st[2 * j], phid = st[2 * j + 1];
+        orc_sincos(phi, &s[j], &c[j]);
+        w[j] = phid * phid;
+    }
+    /* mass matrix, upper triangle */
+    A[0][0] = k->m00;
+    for (uint32_t j = 1; j <= N; ++j) {
+        A[0][j] = k->h[j] * c[j];
+        A[j][j] = k->g_diag[j];
+    }
+    for (uint32_t j = 1; j <= N; ++j)
+        for (uint32_t i = j + 1; i <= N; ++i) {
+            float ss = s[j] * s[i];
+            float cjk = fmaf(c[j], c[i], ss);             /* cos(phi_j - phi_i) */
+            A[j][i] = k->lh[i] * cjk;
+        }
+    /* forces */
+    f[0] = force;
+    for (uint32_t j = 1; j <= N; ++j) {
+        float hs = k->h[j] * s[j];
+        f[0] = fmaf(hs, w[j], f[0]);                      /* + h_j sin(phi_j) phid_j^2 */
+    }
+    for (uint32_t j = 1; j <= N; ++j) f[j] = k->gh[j] * s[j];
+    for (uint32_t j = 1; j <= N; ++j)
+        for (uint32_t i = j + 1; i <= N; ++i) {
+            float cs = c[j] * s[i];
+            float sjk = fmaf(s[j], c[i], -cs);            /* sin(phi_j - phi_i) */
+            float P = k->lh[i] * sjk;                     /* G_ji sin(phi_j - phi_i) */
+            f[j] = fmaf(-P, w[i], f[j]);
+            f[i] = fmaf(P, w[j], f[i]);                   /* sin(phi_i - phi_j) = -sjk */
+        }
+    /* elimination on the upper triangle */
+    for (uint32_t p = 0; p + 1 < S; ++p) {
+        inv[p] = 1.0f / A[p][p];
+        for (uint32_t i = p + 1; i < S; ++i) {
+            float l = A[p][i] * inv[p];
+            for (uint32_t j = i; j < S; ++j) A[i][j] = fmaf(-l, A[p][j], A[i][j]);
+            f[i] = fmaf(-l, f[p], f[i]);
+        }
+    }
+    inv[S - 1] = 1.0f / A[S - 1][S - 1];
+    /* back substitution */
+    for (uint32_t ii = S; ii-- > 0;) {
+        float acc = f[ii];
+        for (uint32_t j = ii + 1; j < S; ++j) acc = fmaf(-A[ii][j], qdd[j], acc);
+        qdd[ii] = acc * inv[ii];
+    }
+}
+
+/* One explicit-Euler iteration of length tau; a == 1 pushes towards +x. */
+void orc_chain_euler(const orc_chain_consts* k, float tau, float force_mag, const float* in, int action, float* out)
+{
+    uint32_t N = k->N;
+    float qdd[ORC_CHAIN_MAX_LINKS + 1];
+    float force = action ? force_mag : -force_mag;
+    orc_chain_accel(k, in, force, qdd);
+    for (uint32_t j = 0; j <= N; ++j) {
+        out[2 * j] = fmaf(tau, in[2 * j + 1], in[2 * j]);
+        out[2 * j + 1] = fmaf(tau, qdd[j], in[2 * j + 1]);
+    }
+}
+
+/* One simulation step: compute_factor C iterations of tau / C, the action held. */
+void orc_chain_env_step(const orc_params* p, const orc_chain_consts* k, const float* in, int action, float* out)
+{
+    uint32_t C = p->compute_factor, S = 2 * (k->N + 1);
+    float sub_tau = p->tau / (float)C;
+    float cur[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+    for (uint32_t q = 0; q < S; ++q) cur[q] = in[q];
+    for (uint32_t c = 0; c < C; ++c) {
+        float nxt[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+        orc_chain_euler(k, sub_tau, p->force_mag, cur, action, nxt);
+        for (uint32_t q = 0; q < S; ++q) cur[q] = nxt[q];
+    }
+    for (uint32_t q = 0; q < S; ++q) out[q] = cur[q];
+}
+
+/* Strict thresholds on the cart position and on every link angle. */
+int orc_chain_terminated(const orc_params* p, uint32_t N, const float* st)
+{
+    if (p->no_termination) return 0;
+    float x = st[0];
+    int out = (x < -p->x_threshold) || (x > p->x_threshold);
+    for (uint32_t j = 1; j <= N; ++j) {
+        float phi = st[2 * j];
+        out |= (phi < -p->theta_threshold_rad) || (phi > p->theta_threshold_rad);
+    }
+    return out;
+}
+
+/* Initial state of an episode that begins at global step t: stream RESET,    */
+/* counter (env, t / 8, RESET, j) for j = 0, 1, ... supplying the 2N + 2      */
+/* state words four at a time in state order.  Episodes of one env that begin */
+/* in the same 8-step block would share a draw; with the default constants    */
+/* none lasts fewer than 8 steps.                                             */
+#define ORC_CHAIN_RESET_SHIFT 3u
+void orc_chain_reset_draw(const orc_params* p, uint32_t N, uint64_t seed, uint32_t env, uint32_t t, float* out)
+{
+    uint32_t S = 2 * (N + 1);
+    uint32_t key[2] = { (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32) };
+    for (uint32_t j = 0; 4 * j < S; ++j) {
+        uint32_t ctr[4] = { env, t >> ORC_CHAIN_RESET_SHIFT, ORC_STREAM_RESET, j };
+        uint32_t w[4];
+        orc_philox4x32_10(ctr, key, w);
+        for (uint32_t q = 0; q < 4 && 4 * j + q < S; ++q) out[4 * j + q] = orc_uniform(w[q], p->reset_low, p->reset_high);
+    }
+}
+
+/* The vectorised chain simulator: n environments with global ids env0 ..,    */
+/* each 2N + 2 state words [S][n] and an episode step counter; random         */
+/* actions, auto-reset, per-256-env block statistics as orc_step.            */
+typedef struct {
+    uint32_t n, env0, N;
+    orc_params p;
+    orc_chain_consts k;
+    uint64_t seed;
+    uint32_t t;
+    int has_reset;
+    float* st;            /* [2N+2][n] */
+    uint32_t* ep;         /* [n] */
+} orc_chain_sim;
+
+void orc_chain_destroy(orc_chain_sim* sim)
+{
+    if (!sim) return;
+    free(sim->st); free(sim->ep);
+    free(sim);
+}
+
+orc_chain_sim* orc_chain_create(uint32_t n, uint32_t env0, uint32_t N, const orc_params* p)
+{
+    if (n == 0 || p->compute_factor == 0 || N < 1 || N > ORC_CHAIN_MAX_LINKS) return NULL;
+    orc_chain_sim* sim = (orc_chain_sim*)calloc(1, sizeof(orc_chain_sim));
+    if (!sim) return NULL;
+    sim->n = n; sim->env0 = env0; sim->N = N; sim->p = *p;
+    orc_chain_make_consts(p, N, &sim->k);
+    sim->st = (float*)calloc((size_t)2 * (N + 1) * n, sizeof(float));
+    sim->ep = (uint32_t*)calloc(n, sizeof(uint32_t));
+    if (!sim->st || !sim->ep) { orc_chain_destroy(sim); return NULL; }
+    return sim;
+}
+
+void orc_chain_reset(orc_chain_sim* sim, uint64_t seed)
+{
+    uint32_t n = sim->n, S = 2 * (sim->N + 1);
+    sim->seed = seed;
+    sim->t = 0;
+    sim->has_reset = 1;
+    for (uint32_t i = 0; i < n; ++i) {
+        float init[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+        orc_chain_reset_draw(&sim->p, sim->N, seed, sim->env0 + i, 0u, init);
+        for (uint32_t q = 0; q < S; ++q) sim->st[(size_t)q * n + i] = init[q];
+        sim->ep[i] = 0;
+    }
+}
+
+/* K steps of every environment; outputs as orc_step with obs [K][S][n]. */
+int orc_chain_step(orc_chain_sim* sim, uint32_t K, float* obs, uint8_t* act, float* rew, uint8_t* done,
+                   uint32_t* stats)
+{
+    if (!sim->has_reset) return -1;
+    if ((uint64_t)sim->t + (uint64_t)K > 0xFFFFFFFFull) return -2;
+    uint32_t n = sim->n, N = sim->N, S = 2 * (N + 1);
+    uint32_t blk0 = sim->env0 / 256u;
+    if (stats) {
+        uint32_t nblk = (sim->env0 + n - 1u) / 256u - blk0 + 1u;
+        memset(stats, 0, (size_t)nblk * 4u * sizeof(uint32_t));
+    }
+    for (uint32_t k = 0; k < K; ++k) {
+        uint32_t t = sim->t + k;
+        for (uint32_t i = 0; i < n; ++i) {
+            uint32_t env = sim->env0 + i;
+            float cur[2 * (ORC_CHAIN_MAX_LINKS + 1)], nxt[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+            for (uint32_t q = 0; q < S; ++q) cur[q] = sim->st[(size_t)q * n + i];
+            int a = orc_action_bit(sim->seed, env, t);
+            orc_chain_env_step(&sim->p, &sim->k, cur, a, nxt);
+            uint32_t len = sim->ep[i] + 1u;
+            int term = orc_chain_terminated(&sim->p, N, nxt);
+            int trunc = (sim->p.max_episode_steps != 0u) && (len >= sim->p.max_episode_steps);
+            uint8_t d = (uint8_t)(term | (trunc << 1));
+            if (obs) for (uint32_t q = 0; q < S; ++q) obs[((size_t)k * S + q) * n + i] = cur[q];
+            if (act) act[(size_t)k * n + i] = (uint8_t)a;
+            if (rew) rew[(size_t)k * n + i] = 1.0f;
+            if (done) done[(size_t)k * n + i] = d;
+            if (d) {
+                orc_chain_reset_draw(&sim->p, N, sim->seed, env, t + 1u, nxt);
+                sim->ep[i] = 0;
+                if (stats) {
+                    uint32_t* sb = stats + (size_t)(env / 256u - blk0) * 4u;
+                    sb[0] += 1u;
+                    sb[1] += len;
+                    sb[2] += (uint32_t)term;
+                    sb[3] += (uint32_t)trunc;
+                }
+            } else {
+                sim->ep[i] = len;
+            }
+            for (uint32_t q = 0; q < S; ++q) sim->st[(size_t)q * n + i] = nxt[q];
+        }
+    }
+    sim->t += K;
+    return 0;
+}
+
+void orc_chain_get_state(const orc_chain_sim* sim, float* st, uint32_t* ep, uint64_t* t)
+{
+    size_t n = sim->n, S = 2 * (sim->N + 1);
+    if (st) memcpy(st, sim->st, S * n * sizeof(float));
+    if (ep) memcpy(ep, sim->ep, n * sizeof(uint32_t));
+    if (t) *t = sim->t;
+}
+
+int orc_chain_set_state(orc_chain_sim* sim, const float* st, const uint32_t* ep, uint64_t t)
+{
+    if (!sim->has_reset) return -1;
+    if (t > 0xFFFFFFFFull) return -2;
+    size_t n = sim->n, S = 2 * (sim->N + 1);
+    if (st) memcpy(sim->st, st, S * n * sizeof(float));
+    if (ep) memcpy(sim->ep, ep, n * sizeof(uint32_t));
+    sim->t = (uint32_t)t;
+    return 0;
+}
+
+/* Teacher-forced check of recorded chain rows ([K][S][n] obs, [K][n] action, */
+/* reward, done), with the same rules, options and return values as          */
+/* orc_check_rows.                                                            */
+uint64_t orc_chain_check_rows(const orc_params* p, uint32_t N, uint64_t seed, uint32_t env0, uint32_t n, uint32_t t0,
+                              uint32_t K, const uint32_t* ep0, const float* obs, const uint8_t* act, const float* rew,
+                              const uint8_t* done, const float* final_state, const uint32_t* final_ep,
+                              uint32_t* bad_k, uint32_t* bad_i)
+{
+    orc_chain_consts kc;
+    if (orc_chain_make_consts(p, N, &kc) != 0) return (uint64_t)-1;
+    uint32_t S = 2 * (N + 1);
+    uint64_t bad = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        uint32_t ep = ep0 ? ep0[i] : 0u;
+        uint32_t env = env0 + i;
+        for (uint32_t k = 0; k < K; ++k) {
+            uint32_t t = t0 + k;
+            float cur[2 * (ORC_CHAIN_MAX_LINKS + 1)], nxt[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+            for (uint32_t q = 0; q < S; ++q) cur[q] = obs[((size_t)k * S + q) * n + i];
+            int ok = 1;
+            if (k == 0 && !ep0) {
+                float start[2 * (ORC_CHAIN_MAX_LINKS + 1)];
+                orc_chain_reset_draw(p, N, seed, env, t0, start);
+                if (memcmp(start, cur, S * sizeof(float)) != 0) ok = 0;
+            }
+            int a = orc_action_bit(seed, env, t);
+            orc_chain_env_step(p, &kc, cur, a, nxt);
+            uint32_t len = ep + 1u;
+            int term = orc_chain_terminated(p, N, nxt);
+            int trunc = (p->max_episode_steps != 0u) && (len >= p->max_episode_steps);
+            uint8_t d = (uint8_t)(term | (trunc << 1));
+            if (act[(size_t)k * n + i] != (uint8_t)a || rew[(size_t)k * n + i] != 1.0f || done[(size_t)k * n + i] != d)
+                ok = 0;
+            if (d) {
+                orc_chain_reset_draw(p, N, seed, env, t + 1u, nxt);
+                ep = 0u;
+            } else {
+                ep = len;
+            }
+            if (ok && k + 1 < K) {
+                for (uint32_t q = 0; q < S; ++q) {
+                    float g = obs[((size_t)(k + 1) * S + q) * n + i];
+                    if (memcmp(&g, &nxt[q], sizeof(float)) != 0) ok = 0;
+                }
+            }
+            if (ok && k + 1 == K) {
+                for (uint32_t q = 0; q < S && final_state; ++q) {
+                    float g = final_state[(size_t)q * n + i];
+                    if (memcmp(&g, &nxt[q], sizeof(float)) != 0) ok = 0;
+                }
+                if (final_ep && final_ep[i] != ep) ok = 0;
+            }
+            if (!ok) {
+                if (bad == 0 && bad_k && bad_i) {
+                    *bad_k = k;
+                    *bad_i = i;
+                }
+                ++bad;
+            }
+        }
+    }
     return bad;
 }

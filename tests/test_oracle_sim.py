@@ -271,27 +271,39 @@ def test_episodes_last_at_least_eight_steps():
 @pytest.mark.parametrize("over", [{}, {"max_episode_steps": 7}, {"x_threshold": 0.3}, {"compute_factor": 3}])
 def test_row_checker_accepts_oracle_rows_and_finds_planted_errors(over):
     """orc_check_rows (the teacher-forced check GPU tests run at full size) passes
-    the oracle's own trajectory and flags a corrupted obs, action, reward or done
-    at the row and env where it was planted."""
+    the oracle's own trajectory and flags a corrupted obs (row 0, which must be
+    the reset draw, included), action, reward or done at the row and env where it
+    was planted, and a final state or episode counter that is not the last
+    row's successor."""
     params = oracle.make_params(**workloads.cartpole(**over))
     n, T, env0, seed = 97, 60, 1000, 5
     sim = oracle.Sim(n, 0, params, env0=env0)
     sim.reset(seed)
     tr = sim.step(T)
-    assert oracle.check_rows(params, seed, env0, 0, tr["obs"], tr["action"], tr["reward"], tr["done"]) == (0, None)
-    for field, k, i in (("obs", 17, 40), ("action", 3, 96), ("reward", 59, 0), ("done", 30, 13)):
+    fin, fin_ep, _ = sim.get_state()
+    assert oracle.check_rows(params, seed, env0, 0, tr["obs"], tr["action"], tr["reward"], tr["done"],
+                             final_state=fin, final_ep=fin_ep) == (0, None)
+    for field, k, i in (("obs", 17, 40), ("obs", 0, 9), ("action", 3, 96), ("reward", 59, 0), ("done", 30, 13),
+                        ("final", T - 1, 50), ("final_ep", T - 1, 3)):
         bad = {key: tr[key].copy() for key in ("obs", "action", "reward", "done")}
+        fs, fe = fin.copy(), fin_ep.copy()
         if field == "obs":
             bad["obs"][k, 2, i] = np.nextafter(bad["obs"][k, 2, i], np.float32(1))
         elif field == "action":
             bad["action"][k, i] ^= 1
         elif field == "reward":
             bad["reward"][k, i] = 0.5
-        else:
+        elif field == "done":
             bad["done"][k, i] ^= 2
-        count, first = oracle.check_rows(params, seed, env0, 0, bad["obs"], bad["action"], bad["reward"], bad["done"])
-        # an obs error shows at the step that produced it (row k - 1 predicts row k)
-        want_k = k - 1 if field == "obs" else k
+        elif field == "final":
+            fs[0, i] = np.nextafter(fs[0, i], np.float32(-1))
+        else:
+            fe[i] += 1
+        count, first = oracle.check_rows(params, seed, env0, 0, bad["obs"], bad["action"], bad["reward"], bad["done"],
+                                         final_state=fs, final_ep=fe)
+        # an obs error shows at the step that produced it (row k - 1 predicts
+        # row k); row 0 is compared with the reset draw
+        want_k = k - 1 if (field == "obs" and k > 0) else k
         assert count >= 1 and first == (want_k, i), (field, count, first)
     # a later start: rows from step t0 with the episode counters at t0
     st, ep, t = sim.get_state()
@@ -351,7 +363,7 @@ def test_policy_row_checker_accepts_oracle_rows_and_finds_planted_errors(bf16):
                 arr[k, i] = np.nextafter(arr[k, i], np.float32(outward * 10))
             bad, first, _ = check(**{field: arr})
             assert bad == 1 and first == (k, i), (field, edge, bad, first)
-    for field, kk, ii in (("action", 11, 30), ("obs", 25, 7), ("reward", 2, 2), ("done", 30, 44)):
+    for field, kk, ii in (("action", 11, 30), ("obs", 25, 7), ("obs", 0, 60), ("reward", 2, 2), ("done", 30, 44)):
         arr = rows[field].copy()
         if field == "action":
             arr[kk, ii] ^= 1
@@ -362,8 +374,23 @@ def test_policy_row_checker_accepts_oracle_rows_and_finds_planted_errors(bf16):
         else:
             arr[kk, ii] ^= 1
         bad, first, _ = check(**{field: arr})
-        want_k = kk - 1 if field == "obs" else kk
+        want_k = kk - 1 if (field == "obs" and kk > 0) else kk
         assert bad >= 1 and first == (want_k, ii), (field, bad, first)
+    # the state after the last row, and the per-step |p0 - oracle p0| output
+    fin, fin_ep, _ = sim.get_state()
+    r = oracle.check_policy_rows(params, pol, seed, env0, 0, rows["obs"], rows["action"], rows["reward"],
+                                 rows["done"], f["p0"], policy_bounds.errs(), logp=f["logp"], value=f["value"],
+                                 final_state=fin, final_ep=fin_ep)
+    assert r[0] == 0
+    fs = fin.copy()
+    fs[2, 17] = np.nextafter(fs[2, 17], np.float32(1))
+    r = oracle.check_policy_rows(params, pol, seed, env0, 0, rows["obs"], rows["action"], rows["reward"],
+                                 rows["done"], f["p0"], policy_bounds.errs(), final_state=fs, final_ep=fin_ep)
+    assert r[:2] == (1, (T - 1, 17))
+    dp0 = np.zeros((T, n), dtype=np.float32)
+    oracle.check_policy_rows(params, pol, seed, env0, 0, rows["obs"], rows["action"], rows["reward"], rows["done"],
+                             f["p0"], policy_bounds.errs(), dp0_out=dp0)
+    assert np.array_equal(dp0, np.abs(f["p0"].astype(np.float64) - tr["p0"]).astype(np.float32))
     # an action flip on the last row (nothing after it to diverge): record p0
     # just across u with the flipped action, its done byte and its log pi
     k = T - 1
