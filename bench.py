@@ -477,9 +477,11 @@ def policy_only(dtype: str, steps: int, warmup: int) -> int:
     return 0
 
 
-def wide_only(D: int, steps: int, warmup: int) -> int:
+def wide_only(D: int, steps: int, warmup: int, copy_calibration: bool = False) -> int:
     """Timed K = 500 launches of the state-size workload alone (for profiling):
-    262,144 envs x 500 steps with D padding words, trajectory recorded."""
+    262,144 envs x 500 steps with D padding words, trajectory recorded; with
+    copy_calibration, then one plain device copy that calibrates the HBM byte
+    counters."""
     import torch
     from paper_2207_07736_amd import Simulator, Trajectory
     w = workloads.WORKLOADS[workloads.STATE_SWEEP]
@@ -506,7 +508,21 @@ def wide_only(D: int, steps: int, warmup: int) -> int:
                       "valu_frac": updates / (ms * 1e-3) / VALU_LANE_OPS_PER_S}), flush=True)
     del traj
     sim.close()
+    if copy_calibration:
+        copy_for_calibration()
     return 0
+
+
+def copy_for_calibration() -> None:
+    """One plain device copy of COPY_BYTES: what the HBM byte counters read for
+    it scales their readings of the kernels."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def unfused_only(steps: int, warmup: int, copy_calibration: bool) -> int:
@@ -541,11 +557,7 @@ def unfused_only(steps: int, warmup: int, copy_calibration: bool) -> int:
     del traj
     sim.close()
     if copy_calibration:
-        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        copy_for_calibration()
     return 0
 
 
@@ -632,7 +644,7 @@ def main() -> int:
     if args.policy:
         return policy_only(args.policy, args.steps, args.warmup)
     if args.wide:
-        return wide_only(args.wide, args.steps, args.warmup)
+        return wide_only(args.wide, args.steps, args.warmup, args.copy_calibration)
     if args.unfused:
         return unfused_only(args.steps, args.warmup, args.copy_calibration)
 
@@ -755,12 +767,7 @@ def main() -> int:
     sim.close()
 
     if args.copy_calibration:
-        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_for_calibration()
 
     if not args.no_sweep:
         result["sweeps"] = fusion_sweeps(stream)
