@@ -5,4 +5,4 @@ include/rlsim.h); ``rlsim`` is its thin ctypes binding.  Importing this package
 loads the library and fails if it has not been built.
 """
 from .rlsim import *  # noqa: F401,F403
-from .rlsim import EXPORTS, LIB_PATH, RlsimError, Simulator, Trajectory  # noqa: F401
+from .rlsim import EXPORTS, LIB_PATH, RlsimError, Simulator, Trajectory, TrajRows, stats_only  # noqa: F401

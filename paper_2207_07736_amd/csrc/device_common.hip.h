@@ -23,20 +23,22 @@ struct DevParams {
     float reset_lo, reset_width;   // width = reset_high - reset_low
     float reset_width_u24;         // width * 2^-24 (exact; see uniform24_to)
     uint32_t key0, key1;  // Philox key: low and high word of the seed
+    uint32_t env0;        // global id of the handle's environment 0 (RNG counters use global ids)
 };
 
 // Counter stream ids (third counter word).
 enum : uint32_t { STREAM_RESET = 0u, STREAM_ACTION = 1u, STREAM_PARAMS = 2u, STREAM_POLICY = 3u };
 
-// Philox4x32-10 (Salmon et al., SC'11) on counter (c0, c1, c2, 0) and key
-// (k0, k1).  c1, c2 and the key are wave-uniform in every caller, so the first
-// round's second product and the whole key schedule land on the scalar unit.
-__device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t k0, uint32_t k1)
+// Philox4x32-10 (Salmon et al., SC'11) on counter (c0, c1, c2, c3) and key
+// (k0, k1).  c1, c2, c3 and the key are wave-uniform in every caller, so the
+// first round's second product and the whole key schedule land on the scalar
+// unit.
+__device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t k0, uint32_t k1,
+                                        uint32_t c3 = 0u)
 {
     // Recompute the key schedule at every call (scalar adds) rather than let
     // it be hoisted into twenty loop-invariant scalars that spill to VGPR lanes.
     asm volatile("" : "+s"(k0), "+s"(k1));
-    uint32_t c3 = 0u;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         // full 64-bit products: one v_mad_u64_u32 gives both halves
@@ -72,7 +74,7 @@ __device__ __forceinline__ float uniform24_to(uint32_t r, float lo, float width_
 
 // Series sin / cos of degree 9 / 8, Horner form, one rounding per operation.
 // Accurate to < 1 ulp for |th| <= 12 degrees (every pre-step angle of a live
-// episode).
+// episode) and to 2.5e-8 + 2 ulp on |th| <= pi/4.
 __device__ __forceinline__ void sincos_series(float th, float& s, float& c)
 {
     const float s3 = (float)(-1.0 / 6.0), s5 = (float)(1.0 / 120.0);
@@ -90,6 +92,35 @@ __device__ __forceinline__ void sincos_series(float th, float& s, float& c)
     c = __builtin_fmaf(z, qc, 1.0f);
 }
 
+// sin / cos at any angle.  |th| <= fp32(pi/4) (every angle of a live
+// cart-pole episode): the series itself.  Otherwise reduce by quadrants first:
+// k = rint(th * fp32(2/pi)), r = th - k pi/2 with pi/2 = hi + lo in two FMAs
+// (th - k hi is exact: both are multiples of 2^-24 and |th - k hi| < 2), and
+// k mod 4 = k - 4 floor(k / 4) (exact in fp32) picks and signs the series
+// values.  A non-finite th gives NaN.  The rare reduction sits in a branch, so
+// a wave whose lanes all hold small angles skips it.
+__device__ __forceinline__ void sincos_full(float th, float& s, float& c)
+{
+    const float quarter_pi = 0x1.921fb6p-1f;        // fp32(pi/4)
+    if (__builtin_fabsf(th) <= quarter_pi) {
+        sincos_series(th, s, c);
+    } else {
+        const float two_over_pi = 0x1.45f306p-1f;   // fp32(2/pi)
+        const float half_pi_hi = 0x1.921fb6p+0f;    // fp32(pi/2)
+        const float half_pi_lo = -0x1.777a5cp-25f;  // fp32(pi/2 - half_pi_hi)
+        const float k = __builtin_rintf(th * two_over_pi);
+        float r = __builtin_fmaf(-k, half_pi_hi, th);
+        r = __builtin_fmaf(-k, half_pi_lo, r);
+        const float quadrant = k - 4.0f * __builtin_floorf(k * 0.25f);
+        float sr, cr;
+        sincos_series(r, sr, cr);
+        const bool odd = quadrant == 1.0f || quadrant == 3.0f;
+        const float a = odd ? cr : sr, b = odd ? sr : cr;      // sin, cos up to sign
+        s = (quadrant == 2.0f || quadrant == 3.0f) ? -a : a;
+        c = (quadrant == 1.0f || quadrant == 2.0f) ? -b : b;
+    }
+}
+
 // One explicit-Euler step of the frictionless cart with a uniform rod:
 //   thacc = (g sin - cos * temp) / (l (4/3 - m cos^2 / M)),
 //   temp  = (F + m l thd^2 sin) / M,   xacc = temp - (m l / M) thacc cos,
@@ -100,7 +131,7 @@ __device__ __forceinline__ CartState cartpole_step(const DevParams& p, const Car
 {
     const float force = act ? p.force_mag : -p.force_mag;
     float sn, cs;
-    sincos_series(s.th, sn, cs);
+    sincos_full(s.th, sn, cs);
     const float ml_thd2 = p.pole_ml * (s.thd * s.thd);
     const float temp = __builtin_fmaf(ml_thd2, sn, force) * p.inv_total;
     const float num = __builtin_fmaf(-cs, temp, p.gravity * sn);

@@ -56,7 +56,8 @@ __device__ __forceinline__ uint32_t xcd_block()
 template <bool REC, bool STATS>
 struct CartCore {
     const DevParams& p;
-    uint32_t env;
+    uint32_t env;        // environment index within the handle
+    uint32_t gid;        // global environment id: the RNG counters' first word
     CartState s;
     uint32_t ep;
     uint4 aw;            // action words of the current 128-step block
@@ -72,7 +73,7 @@ struct CartCore {
     uint32_t n_eps = 0u, n_term = 0u, n_trunc = 0u;
 
     __device__ __forceinline__ CartCore(const DevParams& p_, uint32_t env_)
-        : p(p_), env(env_), off4(env_ * 4u), off1a(env_), off1d(env_) {}
+        : p(p_), env(env_), gid(env_ + p_.env0), off4(env_ * 4u), off1a(env_), off1d(env_) {}
 
     // Sum of the lengths of the episodes that ended in this launch: every step
     // adds one to the running episode, so the finished lengths plus the final
@@ -81,7 +82,7 @@ struct CartCore {
 
     __device__ __forceinline__ void draw_reset(uint32_t block)
     {
-        const uint4 w = philox(env, block, STREAM_RESET, p.key0, p.key1);
+        const uint4 w = philox(gid, block, STREAM_RESET, p.key0, p.key1);
         rs.x = uniform24_to(w.x, p.reset_lo, p.reset_width_u24);
         rs.xd = uniform24_to(w.y, p.reset_lo, p.reset_width_u24);
         rs.th = uniform24_to(w.z, p.reset_lo, p.reset_width_u24);
@@ -91,7 +92,7 @@ struct CartCore {
     // Called before the step at t when t is a multiple of 32.
     __device__ __forceinline__ void refresh_actions(uint32_t t)
     {
-        if ((t & 127u) == 0u) aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
+        if ((t & 127u) == 0u) aw = philox(gid, t >> 7, STREAM_ACTION, p.key0, p.key1);
         abits = pick_word(aw, (t >> 5) & 3u);
     }
 
@@ -164,7 +165,7 @@ struct CartCore {
     __device__ __forceinline__ void run(uint32_t t0, uint32_t K, Hook& hook)
     {
         uint32_t t = t0, k = 0;
-        aw = philox(env, t >> 7, STREAM_ACTION, p.key0, p.key1);
+        aw = philox(gid, t >> 7, STREAM_ACTION, p.key0, p.key1);
         abits = pick_word(aw, (t >> 5) & 3u) >> (t & 31u);
         if (((t + 1u) & 7u) != 0u) {
             // up to seven steps before the first block boundary; none of them
@@ -466,7 +467,7 @@ __global__ __launch_bounds__(kBlock) void k_reset_cart(DevParams p, uint32_t n, 
 {
     const uint32_t env = blockIdx.x * kBlock + threadIdx.x;
     if (env >= n) return;
-    const uint4 w = philox(env, 0u, STREAM_RESET, p.key0, p.key1);
+    const uint4 w = philox(env + p.env0, 0u, STREAM_RESET, p.key0, p.key1);
     const size_t plane = n;
     cart[env] = uniform01_to(w.x, p.reset_lo, p.reset_width);
     cart[plane + env] = uniform01_to(w.y, p.reset_lo, p.reset_width);
@@ -486,7 +487,7 @@ __global__ __launch_bounds__(kBlock) void k_reset_pad(DevParams p, uint32_t n, u
         // consecutive threads take consecutive addresses in either layout
         const uint32_t env = (uint32_t)(stride_e == 1 ? i % n : i / D);
         const uint32_t j = (uint32_t)(stride_e == 1 ? i / n : i % D);
-        const uint4 w = philox(env, j, STREAM_PARAMS, p.key0, p.key1);
+        const uint4 w = philox(env + p.env0, j, STREAM_PARAMS, p.key0, p.key1);
         const size_t q = (size_t)j * stride_j + (size_t)env * stride_e;
         pa[q] = uniform01_to(w.x, a_lo, a_width);
         pb[q] = uniform01_to(w.y, b_lo, b_width);

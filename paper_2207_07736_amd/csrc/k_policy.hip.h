@@ -407,7 +407,7 @@ __global__ __launch_bounds__(kBlock) void k_policy_fused(StepArgs a, PolicyArgs 
     for (uint32_t k = 0; k < a.K; ++k) {
         const uint32_t t = a.t0 + k;
         if (k == 0u || ((t + 1u) & 7u) == 0u) core.draw_reset((t + 1u) >> 3);
-        if (k == 0u || (t & 3u) == 0u) pw = philox(env, t >> 2, STREAM_POLICY, p.key0, p.key1);
+        if (k == 0u || (t & 3u) == 0u) pw = philox(core.gid, t >> 2, STREAM_POLICY, p.key0, p.key1);
         const float u = u24(pick_word(pw, t & 3u));
         float d, v;
         mlp.template eval<OUT>(core.s, lds_b1, lds_b2, lds_w3, lane, d, v);

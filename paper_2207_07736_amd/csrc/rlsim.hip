@@ -12,6 +12,7 @@
 #include <string>
 #include <vector>
 
+#include "k_chain.hip.h"
 #include "k_policy.hip.h"
 #include "k_wide.hip.h"
 
@@ -20,13 +21,17 @@ using namespace rlsim_dev;
 struct rlsim {
     uint32_t n = 0;             // environments
     uint32_t D = 0;             // padding words per environment
+    uint32_t model = RLSIM_MODEL_CARTPOLE;
+    uint32_t links = 0;         // chain links N (chain model)
+    uint32_t S = 4;             // simulator state words: 4, or 2N + 2 for the chain
     int device = 0;
     hipStream_t stream = nullptr;
     rlsim_cfg cfg{};
     DevParams dp{};
+    ChainParams cp{};           // chain model: couplings (cp.p == dp)
     uint64_t t = 0;             // global step of the next step
     bool has_reset = false;
-    float* cart = nullptr;      // [4][n]
+    float* cart = nullptr;      // [S][n]
     uint32_t* ep = nullptr;     // [n]
     bool wide = false;          // padding layout: false [D][n], true [n][Dp]
     uint32_t Dp = 0;            // wide row length (D rounded up to a multiple of 4)
@@ -100,7 +105,39 @@ DevParams make_dev_params(const rlsim_cfg& c, uint64_t seed)
     p.reset_width_u24 = std::ldexp((float)width, -24);   // exact: check_cfg bounds the width
     p.key0 = (uint32_t)(seed & 0xFFFFFFFFull);
     p.key1 = (uint32_t)(seed >> 32);
+    p.env0 = c.env0;
     return p;
+}
+
+// The chain's couplings, each one fp32 operation on the configured values,
+// in the order the kernel's definition fixes: L = 2 l, mu_k = (N - k) m,
+// h_k = L (m/2 + mu_k), G_kk = (L L)(m/3 + mu_k), L h_k, g h_k, mc + N m.
+ChainParams make_chain_params(const rlsim_cfg& c, uint32_t N, const DevParams& dp)
+{
+    ChainParams cp{};
+    cp.p = dp;
+    const float m = c.masspole;
+    volatile float L = 2.0f * c.half_length;
+    volatile float LL = L * L;
+    volatile float half_m = 0.5f * m;
+    volatile float third_m = m / 3.0f;
+    for (uint32_t j = 1; j <= N; ++j) {
+        volatile float mu = (float)(N - j) * m;
+        volatile float hm = half_m + mu;
+        volatile float h = L * hm;
+        volatile float gm = third_m + mu;
+        volatile float gd = LL * gm;
+        volatile float lh = L * h;
+        volatile float gh = c.gravity * h;
+        cp.h[j] = h;
+        cp.gdiag[j] = gd;
+        cp.lh[j] = lh;
+        cp.gh[j] = gh;
+    }
+    volatile float nm = (float)N * m;
+    volatile float m00 = c.masscart + nm;
+    cp.m00 = m00;
+    return cp;
 }
 
 const char* check_cfg(const rlsim_cfg& c)
@@ -123,6 +160,10 @@ const char* check_cfg(const rlsim_cfg& c)
     if (c.pad_a_low > c.pad_a_high || c.pad_b_low > c.pad_b_high) return "cfg: padding range low > high";
     if ((c.flags & ~(uint32_t)RLSIM_F_NO_TERMINATION) != 0u) return "cfg: unknown flag bits";
     if (c.compute_factor == 0u) return "cfg: compute_factor must be >= 1";
+    if (c.env0 % 256u != 0u) return "cfg: env0 must be a multiple of 256";
+    if (c.model != RLSIM_MODEL_CARTPOLE && c.model != RLSIM_MODEL_CHAIN) return "cfg: unknown model";
+    if (c.model == RLSIM_MODEL_CHAIN && (c.n_links < 1u || c.n_links > (uint32_t)kMaxLinks))
+        return "cfg: n_links must be in [1, 4] for the chain model";
     return nullptr;
 }
 
@@ -204,6 +245,31 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
     return hipGetLastError();
 }
 
+template <bool REC, bool STATS>
+hipError_t launch_chain(const ChainArgs& a, uint32_t N, hipStream_t s)
+{
+    const dim3 grid(grid_for(a.n)), block(kBlock);
+    switch (N) {
+    case 1: hipLaunchKernelGGL((k_chain_fused<1, REC, STATS>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_chain_fused<2, REC, STATS>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_chain_fused<3, REC, STATS>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_chain_fused<4, REC, STATS>), grid, block, 0, s, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_chain_reset(const DevParams& p, uint32_t N, uint32_t n, float* state, uint32_t* ep, hipStream_t s)
+{
+    const dim3 grid(grid_for(n)), block(kBlock);
+    switch (N) {
+    case 1: hipLaunchKernelGGL(k_reset_chain<1>, grid, block, 0, s, p, n, state, ep); break;
+    case 2: hipLaunchKernelGGL(k_reset_chain<2>, grid, block, 0, s, p, n, state, ep); break;
+    case 3: hipLaunchKernelGGL(k_reset_chain<3>, grid, block, 0, s, p, n, state, ep); break;
+    default: hipLaunchKernelGGL(k_reset_chain<4>, grid, block, 0, s, p, n, state, ep); break;
+    }
+    return hipGetLastError();
+}
+
 template <class Mlp, bool REC, bool STATS>
 hipError_t launch_policy(const StepArgs& a, const PolicyArgs& w, hipStream_t s)
 {
@@ -246,6 +312,9 @@ void rlsim_cfg_default(rlsim_cfg* c)
     c->pad_b_high = 1.0f;
     c->flags = 0u;
     c->compute_factor = 1u;
+    c->env0 = 0u;
+    c->model = RLSIM_MODEL_CARTPOLE;
+    c->n_links = 0u;
     c->stream = nullptr;
 }
 
@@ -260,12 +329,21 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
     if (cfg) c = *cfg;
     else rlsim_cfg_default(&c);
     if (const char* why = check_cfg(c)) return fail(nullptr, RLSIM_EINVAL, std::string("rlsim_create: ") + why);
-    const uint32_t D = state_words - 4u;
+    if ((uint64_t)c.env0 + n_envs > (1ull << 32))
+        return fail(nullptr, RLSIM_EINVAL, "rlsim_create: env0 + n_envs must be <= 2^32 (global ids are 32-bit)");
+    const bool chain = c.model == RLSIM_MODEL_CHAIN;
+    const uint32_t S = chain ? 2u * (c.n_links + 1u) : 4u;
+    if (chain && state_words != S)
+        return fail(nullptr, RLSIM_EINVAL, "rlsim_create: the chain model takes state_words = 2 n_links + 2");
+    const uint32_t D = state_words - S;
 
     rlsim* h = new (std::nothrow) rlsim();
     if (!h) return fail(nullptr, RLSIM_ENOMEM, "rlsim_create: host allocation failed");
     h->n = n_envs;
     h->D = D;
+    h->model = c.model;
+    h->links = chain ? c.n_links : 0u;
+    h->S = S;
     h->wide = D > kMaxRegisterWords;
     h->Dp = h->wide ? (D + 3u) & ~3u : D;
     h->cfg = c;
@@ -277,7 +355,7 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
         return rc;
     }
     const size_t n = n_envs;
-    e = hipMalloc(&h->cart, 4 * n * sizeof(float));
+    e = hipMalloc(&h->cart, (size_t)S * n * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&h->ep, n * sizeof(uint32_t));
     const size_t pad_bytes = (size_t)h->Dp * n * sizeof(float);
     if (e == hipSuccess && D) e = hipMalloc(&h->pad_s, pad_bytes);
@@ -305,8 +383,15 @@ int rlsim_reset(rlsim_t* h, uint64_t seed)
     DeviceGuard g(h->device);
     if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_reset: cannot select the handle's device");
     h->dp = make_dev_params(h->cfg, seed);
-    hipLaunchKernelGGL(k_reset_cart, dim3(grid_for(h->n)), dim3(kBlock), 0, h->stream, h->dp, h->n, h->cart, h->ep);
-    hipError_t e = hipGetLastError();
+    hipError_t e;
+    if (h->model == RLSIM_MODEL_CHAIN) {
+        h->cp = make_chain_params(h->cfg, h->links, h->dp);
+        e = launch_chain_reset(h->dp, h->links, h->n, h->cart, h->ep, h->stream);
+    } else {
+        hipLaunchKernelGGL(k_reset_cart, dim3(grid_for(h->n)), dim3(kBlock), 0, h->stream, h->dp, h->n, h->cart,
+                           h->ep);
+        e = hipGetLastError();
+    }
     if (e != hipSuccess) return hip_fail(h, e, "rlsim_reset: launch");
     if (h->D) {
         volatile float a_w = h->cfg.pad_a_high - h->cfg.pad_a_low;
@@ -356,10 +441,35 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
             return fail(h, RLSIM_EINVAL, "rlsim_step_fused: misaligned policy arrays");
         if (h->D != 0u)
             return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: a policy with padding words is not supported");
+        if (h->model != RLSIM_MODEL_CARTPOLE)
+            return fail(h, RLSIM_EUNSUPPORTED, "rlsim_step_fused: the MLP policy reads the cart-pole's 4 state words");
     }
 
     DeviceGuard g(h->device);
     if (!g.ok) return fail(h, RLSIM_EDEVICE, "rlsim_step_fused: cannot select the handle's device");
+    const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
+    hipError_t e;
+    if (h->model == RLSIM_MODEL_CHAIN) {
+        ChainArgs ca{};
+        ca.c = h->cp;
+        ca.n = h->n;
+        ca.t0 = (uint32_t)h->t;
+        ca.K = K;
+        ca.state = h->cart;
+        ca.ep = h->ep;
+        ca.obs = tr.obs;
+        ca.action = tr.action;
+        ca.reward = tr.reward;
+        ca.done = tr.done;
+        ca.stats = tr.block_stats;
+        if (rec && stats) e = launch_chain<true, true>(ca, h->links, h->stream);
+        else if (rec) e = launch_chain<true, false>(ca, h->links, h->stream);
+        else if (stats) e = launch_chain<false, true>(ca, h->links, h->stream);
+        else e = launch_chain<false, false>(ca, h->links, h->stream);
+        if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");
+        h->t += K;
+        return RLSIM_OK;
+    }
     StepArgs a{};
     a.p = h->dp;
     a.n = h->n;
@@ -377,8 +487,6 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
     a.reward = tr.reward;
     a.done = tr.done;
     a.stats = tr.block_stats;
-    const bool rec = n_set == 4, stats = tr.block_stats != nullptr;
-    hipError_t e;
     if (policy) {
         PolicyArgs w{policy->w1, policy->b1, policy->w2, policy->b2, policy->w3, policy->b3,
                      policy->wv, policy->bv, tr.policy_p0, tr.logp, tr.value};
@@ -407,9 +515,9 @@ int rlsim_get_state(rlsim_t* h, float* host_state, uint32_t* host_ep, uint64_t* 
     std::vector<float> rows;     // wide layout staging, [n][Dp]
     hipError_t e = hipSuccess;
     if (host_state) {
-        e = hipMemcpyAsync(host_state, h->cart, 4 * n * sizeof(float), hipMemcpyDeviceToHost, h->stream);
+        e = hipMemcpyAsync(host_state, h->cart, (size_t)h->S * n * sizeof(float), hipMemcpyDeviceToHost, h->stream);
         if (e == hipSuccess && h->D && !h->wide)
-            e = hipMemcpyAsync(host_state + 4 * n, h->pad_s, (size_t)h->D * n * sizeof(float), hipMemcpyDeviceToHost,
+            e = hipMemcpyAsync(host_state + (size_t)h->S * n, h->pad_s, (size_t)h->D * n * sizeof(float), hipMemcpyDeviceToHost,
                                h->stream);
         if (e == hipSuccess && h->wide) {
             try {
@@ -423,7 +531,7 @@ int rlsim_get_state(rlsim_t* h, float* host_state, uint32_t* host_ep, uint64_t* 
     if (e == hipSuccess && host_ep) e = hipMemcpyAsync(host_ep, h->ep, n * sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "rlsim_get_state");
-    if (host_state && h->wide) transpose_rows_to_planes(rows.data(), host_state + 4 * n, n, h->D, h->Dp);
+    if (host_state && h->wide) transpose_rows_to_planes(rows.data(), host_state + (size_t)h->S * n, n, h->D, h->Dp);
     if (t_out) *t_out = h->t;
     return RLSIM_OK;
 }
@@ -443,13 +551,13 @@ int rlsim_set_state(rlsim_t* h, const float* host_state, const uint32_t* host_ep
         } catch (const std::bad_alloc&) {
             return fail(h, RLSIM_ENOMEM, "rlsim_set_state: host staging allocation failed");
         }
-        transpose_planes_to_rows(host_state + 4 * n, rows.data(), n, h->D, h->Dp);
+        transpose_planes_to_rows(host_state + (size_t)h->S * n, rows.data(), n, h->D, h->Dp);
     }
     hipError_t e = hipSuccess;
     if (host_state) {
-        e = hipMemcpyAsync(h->cart, host_state, 4 * n * sizeof(float), hipMemcpyHostToDevice, h->stream);
+        e = hipMemcpyAsync(h->cart, host_state, (size_t)h->S * n * sizeof(float), hipMemcpyHostToDevice, h->stream);
         if (e == hipSuccess && h->D && !h->wide)
-            e = hipMemcpyAsync(h->pad_s, host_state + 4 * n, (size_t)h->D * n * sizeof(float), hipMemcpyHostToDevice,
+            e = hipMemcpyAsync(h->pad_s, host_state + (size_t)h->S * n, (size_t)h->D * n * sizeof(float), hipMemcpyHostToDevice,
                                h->stream);
         if (e == hipSuccess && h->wide)
             e = hipMemcpyAsync(h->pad_s, rows.data(), rows.size() * sizeof(float), hipMemcpyHostToDevice, h->stream);

@@ -23,6 +23,8 @@ RLSIM_EUNSUPPORTED = -5
 RLSIM_F32 = 0
 RLSIM_BF16 = 1
 RLSIM_F_NO_TERMINATION = 1
+RLSIM_MODEL_CARTPOLE = 0
+RLSIM_MODEL_CHAIN = 1
 
 # every entry point include/rlsim.h declares
 EXPORTS = ("rlsim_cfg_default", "rlsim_create", "rlsim_reset", "rlsim_step_fused", "rlsim_get_state",
@@ -46,6 +48,9 @@ class rlsim_cfg(ctypes.Structure):
         ("pad_b_low", ctypes.c_float), ("pad_b_high", ctypes.c_float),
         ("flags", ctypes.c_uint32),
         ("compute_factor", ctypes.c_uint32),
+        ("env0", ctypes.c_uint32),
+        ("model", ctypes.c_uint32),
+        ("n_links", ctypes.c_uint32),
         ("stream", ctypes.c_void_p),
     ]
 
@@ -183,14 +188,55 @@ def policy_struct(dtype: int, w1, b1, w2, b2, w3, b3, wv=None, bv=None) -> rlsim
     return rlsim_policy(int(dtype), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(w3), _ptr(b3), _ptr(wv), _ptr(bv))
 
 
+class TrajRows:
+    """The rows one rlsim_step_fused call records, with the shape they were cut
+    for: ``struct`` (the C struct), ``K`` steps (None for a statistics-only
+    record, which suits any K), ``n`` environments and ``S`` state words.
+    Simulator.step checks the shape against the call before anything is
+    enqueued, so a mismatch raises instead of letting a kernel write past a
+    buffer.  An output plane can be switched off by setting it to None."""
+
+    _FIELDS = tuple(f for f, _ in rlsim_traj._fields_)
+
+    def __init__(self, struct: rlsim_traj, K, n: int, S):
+        object.__setattr__(self, "struct", struct)
+        object.__setattr__(self, "K", K)
+        object.__setattr__(self, "n", n)
+        object.__setattr__(self, "S", S)
+
+    def __getattr__(self, name):
+        if name in TrajRows._FIELDS:
+            return getattr(self.struct, name)
+        raise AttributeError(name)
+
+    def __setattr__(self, name, value):
+        if name not in TrajRows._FIELDS:
+            raise AttributeError(name)
+        if value is not None:
+            raise ValueError("a recorded plane can only be switched off (set to None)")
+        setattr(self.struct, name, None)
+
+
+def stats_only(block_stats, n: int) -> TrajRows:
+    """A record of the per-256-env block statistics alone (no trajectory rows)
+    for n environments; block_stats is a device tensor of at least
+    ceil(n / 256) x 4 32-bit words."""
+    need = 4 * ((n + 255) // 256)
+    if block_stats.numel() * block_stats.element_size() < 4 * need or not block_stats.is_contiguous():
+        raise ValueError(f"block_stats must hold {need} contiguous 32-bit words")
+    return TrajRows(traj_struct(block_stats=block_stats), None, n, None)
+
+
 class Trajectory:
-    """Device buffers of K trajectory rows for n environments (torch tensors).
+    """Device buffers of K trajectory rows for n environments with S state words
+    each (4 for the cart-pole, 2 N + 2 for an N-link chain), as torch tensors.
     ``learner=True`` adds the per-step log pi(a|obs) and value planes."""
 
-    def __init__(self, K: int, n: int, device="cuda", stats: bool = True, p0: bool = False, learner: bool = False):
+    def __init__(self, K: int, n: int, device="cuda", stats: bool = True, p0: bool = False, learner: bool = False,
+                 S: int = 4):
         import torch
-        self.K, self.n = K, n
-        self.obs = torch.empty((K, 4, n), dtype=torch.float32, device=device)
+        self.K, self.n, self.S = K, n, S
+        self.obs = torch.empty((K, S, n), dtype=torch.float32, device=device)
         self.action = torch.empty((K, n), dtype=torch.uint8, device=device)
         self.reward = torch.empty((K, n), dtype=torch.float32, device=device)
         self.done = torch.empty((K, n), dtype=torch.uint8, device=device)
@@ -199,18 +245,19 @@ class Trajectory:
         self.logp = torch.empty((K, n), dtype=torch.float32, device=device) if learner else None
         self.value = torch.empty((K, n), dtype=torch.float32, device=device) if learner else None
 
-    def rows(self, k0: int, k: int) -> rlsim_traj:
-        """Struct addressing rows k0 .. k0+k-1 (for a call with K = k)."""
-        if k0 < 0 or k0 + k > self.K:
+    def rows(self, k0: int, k: int) -> TrajRows:
+        """Rows k0 .. k0+k-1, for a call with K = k."""
+        if k < 1 or k0 < 0 or k0 + k > self.K:
             raise ValueError("row range outside the trajectory")
         part = lambda x: None if x is None else x[k0:k0 + k]  # noqa: E731
-        return traj_struct(self.obs[k0:k0 + k], self.action[k0:k0 + k], self.reward[k0:k0 + k],
-                           self.done[k0:k0 + k], self.block_stats, part(self.policy_p0), part(self.logp),
-                           part(self.value))
+        st = traj_struct(self.obs[k0:k0 + k], self.action[k0:k0 + k], self.reward[k0:k0 + k],
+                         self.done[k0:k0 + k], self.block_stats, part(self.policy_p0), part(self.logp),
+                         part(self.value))
+        return TrajRows(st, k, self.n, self.S)
 
     def learner_batch(self) -> dict:
         """The recorded rows as a learner reads them, as views of the buffers the
-        kernel wrote (no copy): obs [K, n, 4], action, reward, done, and when
+        kernel wrote (no copy): obs [K, n, S], action, reward, done, and when
         recorded logp and value [K, n]."""
         out = dict(obs=self.obs.permute(0, 2, 1), action=self.action, reward=self.reward, done=self.done)
         if self.logp is not None:
@@ -219,12 +266,21 @@ class Trajectory:
 
 
 class Simulator:
-    """Owning wrapper of one rlsim handle (convenience for tests and the bench)."""
+    """Owning wrapper of one rlsim handle (convenience for tests and the bench).
+    ``links`` > 0 selects the chain model with that many links (no padding
+    words); ``env0`` is the handle's first global environment id."""
 
-    def __init__(self, n_envs: int, D: int = 0, cfg_values: dict | None = None, stream=None):
-        self.n, self.D = int(n_envs), int(D)
+    def __init__(self, n_envs: int, D: int = 0, cfg_values: dict | None = None, stream=None, links: int = 0,
+                 env0: int = 0):
+        self.n, self.D, self.links = int(n_envs), int(D), int(links)
         self.cfg = make_cfg(cfg_values, stream)
-        self.h = rlsim_create(self.n, 4 + self.D, self.cfg)
+        self.cfg.env0 = int(env0)
+        if self.links:
+            self.cfg.model, self.cfg.n_links = RLSIM_MODEL_CHAIN, self.links
+            self.S = 2 * (self.links + 1)
+        else:
+            self.S = 4
+        self.h = rlsim_create(self.n, self.S + self.D, self.cfg)
 
     def close(self):
         if self.h:
@@ -240,11 +296,19 @@ class Simulator:
     def reset(self, seed: int):
         rlsim_reset(self.h, seed)
 
-    def step(self, K: int, traj: rlsim_traj | None = None, policy: rlsim_policy | None = None):
-        rlsim_step_fused(self.h, K, policy, traj)
+    def step(self, K: int, traj: TrajRows | None = None, policy: rlsim_policy | None = None):
+        """One rlsim_step_fused call of K steps recording into traj (rows cut
+        for exactly this K and this simulator, or a statistics-only record)."""
+        if traj is not None:
+            if not isinstance(traj, TrajRows):
+                raise TypeError("traj must come from Trajectory.rows() or stats_only()")
+            if traj.n != self.n or (traj.K is not None and (traj.K != K or traj.S != self.S)):
+                raise ValueError(f"rows cut for K={traj.K}, n={traj.n}, S={traj.S}; the call has K={K}, "
+                                 f"n={self.n}, S={self.S}")
+        rlsim_step_fused(self.h, K, policy, None if traj is None else traj.struct)
 
     def get_state(self):
-        return rlsim_get_state(self.h, self.n, 4 + self.D)
+        return rlsim_get_state(self.h, self.n, self.S + self.D)
 
     def set_state(self, state, ep, t):
         rlsim_set_state(self.h, state, ep, t)

@@ -8,13 +8,19 @@ import oracle
 import workloads
 
 
-def oracle_run(n, T, K_schedule, D=0, seed=0, env0=0, cfg=None, policy=None):
+def oracle_run(n, T, K_schedule, D=0, seed=0, env0=0, cfg=None, policy=None, links=0):
     """Oracle trajectory for envs env0..env0+n-1 over T steps, split into calls
-    of the given sizes (stats kept per call)."""
+    of the given sizes (stats kept per call); links > 0 runs the chain model."""
     params = oracle.make_params(**(cfg or workloads.CARTPOLE))
-    sim = oracle.Sim(n, D, params, env0=env0)
-    sim.reset(seed)
-    parts = [sim.step(k, policy=policy) for k in K_schedule]
+    if links:
+        assert D == 0 and policy is None
+        sim = oracle.ChainSim(n, links, params, env0=env0)
+        sim.reset(seed)
+        parts = [sim.step(k) for k in K_schedule]
+    else:
+        sim = oracle.Sim(n, D, params, env0=env0)
+        sim.reset(seed)
+        parts = [sim.step(k, policy=policy) for k in K_schedule]
     assert sum(K_schedule) == T
     out = {key: np.concatenate([p[key] for p in parts]) for key in ("obs", "action", "reward", "done")}
     if policy is not None:
@@ -25,17 +31,18 @@ def oracle_run(n, T, K_schedule, D=0, seed=0, env0=0, cfg=None, policy=None):
 
 
 def gpu_run(n, T, K_schedule, D=0, seed=0, cfg=None, stats=True, stream=None, policy=None, p0=False,
-            slices=None):
-    """GPU trajectory over T steps with the given K schedule.  Returns host
+            slices=None, links=0, env0=0):
+    """GPU trajectory over T steps with the given K schedule (links > 0: the
+    chain model; env0: the handle's first global env id).  Returns host
     arrays; if ``slices`` (list of (start, stop) env ranges) is given, only
     those columns are copied back (for full-size runs)."""
     import torch
     from paper_2207_07736_amd import Simulator, Trajectory
 
-    sim = Simulator(n, D, cfg or workloads.CARTPOLE, stream=stream)
+    sim = Simulator(n, D, cfg or workloads.CARTPOLE, stream=stream, links=links, env0=env0)
     try:
         sim.reset(seed)
-        traj = Trajectory(T, n, stats=stats, p0=p0)
+        traj = Trajectory(T, n, stats=stats, p0=p0, S=sim.S)
         stats_list = []
         k0 = 0
         for k in K_schedule:
@@ -69,11 +76,14 @@ def gpu_run(n, T, K_schedule, D=0, seed=0, cfg=None, stats=True, stream=None, po
 
 
 def assert_bit_equal(gpu, ref, keys=("obs", "action", "reward", "done", "state", "ep")):
+    """Every float equal bit for bit and finite (a NaN on both sides is a
+    failure: only tests that poison the state on purpose compare NaN-ness, with
+    their own check), every integer equal."""
     for key in keys:
         g, r = np.asarray(gpu[key]), np.asarray(ref[key])
         assert g.shape == r.shape, (key, g.shape, r.shape)
         if g.dtype.kind == "f":
-            same = (g.view(np.uint32) == r.view(np.uint32)) | (np.isnan(g) & np.isnan(r))
+            same = (g.view(np.uint32) == r.view(np.uint32)) & np.isfinite(g)
         else:
             same = g == r
         if not np.all(same):

@@ -122,16 +122,16 @@ def test_state_and_argument_errors_with_handle():
         tr = p.Trajectory(4, 300)
         bad = p.traj_struct(obs=tr.obs, action=tr.action)          # mixed NULLs
         with pytest.raises(p.RlsimError) as e:
-            sim.step(4, bad)
+            p.rlsim_step_fused(sim.h, 4, None, bad)
         assert e.value.code == p.RLSIM_EINVAL
         mis = p.rlsim_traj(tr.obs.data_ptr() + 2, tr.action.data_ptr(), tr.reward.data_ptr(), tr.done.data_ptr(),
                            None, None)
         with pytest.raises(p.RlsimError) as e:
-            sim.step(4, mis)
+            p.rlsim_step_fused(sim.h, 4, None, mis)
         assert e.value.code == p.RLSIM_EINVAL
         p0only = p.traj_struct(policy_p0=tr.obs)
         with pytest.raises(p.RlsimError) as e:
-            sim.step(4, p0only)
+            p.rlsim_step_fused(sim.h, 4, None, p0only)
         assert e.value.code == p.RLSIM_EINVAL
         st, ep, t = sim.get_state()
         sim.set_state(st, ep, 2**32 - 5)
@@ -257,3 +257,50 @@ def test_create_rejects_every_invalid_cfg_drawn():
         rc = p.lib.rlsim_create(16, 4, ctypes.byref(c), ctypes.byref(h))
         assert rc == p.RLSIM_EINVAL and not h.value, (kind, rc)
         assert p.rlsim_last_error(None).startswith("rlsim_create: cfg")
+
+
+@pytest.mark.parametrize("env0,n", [(1, 16), (255, 16), (2**32 - 256, 512), (2**32 - 2**20, 2**20 + 1)])
+def test_create_rejects_bad_env0(env0, n):
+    """Global env ids are 32-bit and blocks of 256 envs: env0 must be a multiple
+    of 256 and env0 + n_envs <= 2^32, checked before any device call."""
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    assert c.env0 == 0
+    c.env0 = env0
+    h = ctypes.c_void_p()
+    assert p.lib.rlsim_create(n, 4, ctypes.byref(c), ctypes.byref(h)) == p.RLSIM_EINVAL and not h.value
+    assert "env0" in p.rlsim_last_error(None)
+
+
+@pytest.mark.parametrize("model,links,words", [(2, 0, 4), (1, 0, 2), (1, 5, 12), (1, 2, 4), (1, 2, 7), (1, 1, 5)])
+def test_create_rejects_bad_model_or_chain_shape(model, links, words):
+    """An unknown model, a chain with n_links outside [1, 4], or a chain whose
+    state_words is not 2 n_links + 2 (no padding words) is EINVAL."""
+    import paper_2207_07736_amd as p
+    c = p.rlsim_cfg_default()
+    assert c.model == p.RLSIM_MODEL_CARTPOLE and c.n_links == 0
+    c.model, c.n_links = model, links
+    h = ctypes.c_void_p()
+    assert p.lib.rlsim_create(64, words, ctypes.byref(c), ctypes.byref(h)) == p.RLSIM_EINVAL and not h.value
+    assert p.rlsim_last_error(None).startswith("rlsim_create")
+
+
+def test_trajectory_rows_carry_their_shape():
+    """Rows cut from a Trajectory know the call they fit; statistics-only
+    records check their buffer's size.  (Simulator.step compares them with
+    the call before any launch; tests/test_gpu_parity.py runs that.)"""
+    from paper_2207_07736_amd import rlsim
+    torch = pytest.importorskip("torch")
+    tr = rlsim.Trajectory(10, 300, device="cpu", S=6)
+    r = tr.rows(2, 5)
+    assert (r.K, r.n, r.S) == (5, 300, 6)
+    assert r.obs == tr.obs[2:7].data_ptr()
+    r.logp = None
+    with pytest.raises(ValueError):
+        r.obs = 1234
+    for k0, k in ((0, 0), (8, 3), (-1, 2)):
+        with pytest.raises(ValueError):
+            tr.rows(k0, k)
+    with pytest.raises(ValueError):
+        rlsim.stats_only(torch.zeros((1, 4), dtype=torch.int32), 300)
+    assert rlsim.stats_only(torch.zeros((2, 4), dtype=torch.int32), 300).K is None

@@ -78,11 +78,16 @@ def test_padding_words_bit_exact(D):
     dict(force_mag=0.0, gravity=0.0),
 ])
 def test_edge_configs(overrides):
+    """Edge configurations; with termination disabled the pole swings through
+    every angle (the quadrant-reduced sin/cos), and every state stays finite."""
     cfg = workloads.cartpole(**overrides)
     n, T = 300, 120
     g = gpu_run(n, T, [50, 70], D=2, seed=3, cfg=cfg)
     r = oracle_run(n, T, [50, 70], D=2, seed=3, cfg=cfg)
     assert_bit_equal(g, r)
+    assert np.isfinite(g["obs"]).all() and np.isfinite(g["state"]).all()
+    if overrides.get("no_termination"):
+        assert np.abs(g["obs"][:, 2]).max() > 4.0        # far past the series' own domain
     _stats_equal(g["stats"], r["stats"])
 
 
@@ -141,6 +146,13 @@ def test_headline_whole_batch_properties():
         per_block = per_env.view(-1, 256).sum(dim=1)
         stats = traj.block_stats.to(torch.int64)
         assert torch.equal(stats[:, 0], per_block)
+        # column 1, the summed lengths of the episodes that ended: each env's
+        # ended episodes span from its first step to its last episode end
+        # (episodes start at the reset, t = 0), so their lengths add up to
+        # 1 + the step index of the env's last done byte (0 without one)
+        steps = torch.arange(1, T + 1, device=dn.device, dtype=torch.int64).view(T, 1)
+        last_end = ((dn != 0).to(torch.int64) * steps).max(dim=0).values
+        assert torch.equal(stats[:, 1], last_end.view(-1, 256).sum(dim=1))
         assert torch.equal(stats[:, 2], (dn & 1).sum(dim=0).view(-1, 256).sum(dim=1))
         assert torch.equal(stats[:, 3], (dn >> 1).sum(dim=0).view(-1, 256).sum(dim=1))
         _, ep, t = sim.get_state()
@@ -162,7 +174,7 @@ def test_rerun_deterministic_and_stream():
 
 
 def test_no_trajectory_and_stats_only():
-    from paper_2207_07736_amd import Simulator, traj_struct
+    from paper_2207_07736_amd import Simulator, stats_only
     n, T = 1000, 90
     r = oracle_run(n, T, [T], seed=4)
     sim = Simulator(n, 3, workloads.CARTPOLE)
@@ -172,7 +184,7 @@ def test_no_trajectory_and_stats_only():
         st_a, ep_a, t_a = sim.get_state()
         sim.reset(4)
         stats = torch.zeros(((n + 255) // 256, 4), dtype=torch.int32, device="cuda")
-        sim.step(T, traj_struct(block_stats=stats))
+        sim.step(T, stats_only(stats, n))
         st_b, ep_b, _ = sim.get_state()
     finally:
         sim.close()
@@ -426,3 +438,77 @@ def test_concurrent_handles_on_two_streams_match_solo_runs():
     finally:
         for sim in sims:
             sim.close()
+
+
+@pytest.mark.parametrize("D", [0, 5, 20])
+def test_env0_handle_equals_oracle_slice(D):
+    """A handle holding global environments env0 .. env0 + n - 1 draws the
+    random numbers of those environments: bit-exact against the oracle's slice
+    with the same global ids (trajectory, statistics rows, final state)."""
+    env0, n, T = 3 * 2**20, 700, 90
+    sched = [40, 50]
+    g = gpu_run(n, T, sched, D=D, seed=6, env0=env0)
+    r = oracle_run(n, T, sched, D=D, seed=6, env0=env0)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
+@pytest.mark.parametrize("D", [0, 3, 40])
+def test_shards_equal_the_single_handle(D):
+    """Two handles of 1,024 environments at env0 = 0 and 1,024 record exactly
+    the columns of one 2,048-env handle (the sharding of the path over GPUs,
+    here on one GPU), for random actions, and the last one's statistics rows
+    are rows 4 .. 7 of the whole handle's."""
+    T, sched = 100, [30, 70]
+    whole = gpu_run(2048, T, sched, D=D, seed=12)
+    for env0 in (0, 1024):
+        part = gpu_run(1024, T, sched, D=D, seed=12, env0=env0)
+        cols = {k: (whole[k][..., env0:env0 + 1024] if k != "ep" else whole[k][env0:env0 + 1024])
+                for k in ("obs", "action", "reward", "done", "state", "ep")}
+        cols["t"] = whole["t"]
+        assert_bit_equal(part, cols)
+        for a, b in zip(part["stats"], whole["stats"]):
+            assert np.array_equal(a, b[env0 // 256:env0 // 256 + 4])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_shards_equal_the_single_handle_with_policy(dtype):
+    """As above with the MLP policy sampling the actions (its uniforms are
+    keyed by global env ids too): bit-identical shards."""
+    from gpu_helpers import device_policy, policy_weights
+    st, keep = device_policy(policy_weights(3, bias_scale=0.2), dtype)
+    T, sched = 48, [16, 32]
+    whole = gpu_run(1024, T, sched, seed=4, policy=st, p0=True)
+    part = gpu_run(512, T, sched, seed=4, policy=st, p0=True, env0=512)
+    cols = {k: whole[k][..., 512:] for k in ("obs", "action", "reward", "done", "p0", "state")}
+    cols["ep"], cols["t"] = whole["ep"][512:], whole["t"]
+    assert_bit_equal(part, cols, keys=("obs", "action", "reward", "done", "p0", "state", "ep"))
+    del keep
+
+
+def test_step_rejects_rows_cut_for_another_call():
+    """Rows cut for another K, another environment count or another state size
+    raise before anything is enqueued: the handle's step counter is unchanged
+    and a correct call afterwards matches the oracle."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    n = 300
+    sim = Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(2)
+        tr = Trajectory(200, n)
+        other_n = Trajectory(10, n + 1)
+        other_s = Trajectory(10, n, S=6)
+        for K, rows in ((200, tr.rows(0, 100)), (5, tr.rows(0, 10)), (10, other_n.rows(0, 10)),
+                        (10, other_s.rows(0, 10))):
+            with pytest.raises(ValueError):
+                sim.step(K, rows)
+        with pytest.raises(TypeError):
+            sim.step(10, rows.struct)
+        assert sim.get_state()[2] == 0
+        sim.step(10, tr.rows(0, 10))
+        torch.cuda.synchronize()
+        r = oracle_run(n, 10, [10], seed=2)
+        assert np.array_equal(tr.obs[:10].cpu().numpy().view(np.uint32), r["obs"].view(np.uint32))
+        del tr, other_n, other_s
+    finally:
+        sim.close()

@@ -71,11 +71,22 @@ WORKLOADS = {
 # iterations per step at a fixed state size, fused against unfused.
 C_SWEEP = dict(name="cartpole-64k-100-Csweep", n=65536, T=100, K=[1, 100], C=[1, 4, 16, 64, 256, 1024], seed=0)
 
+# The second simulator (the paper's Future Work: heavier, multi-body
+# simulators): a cart carrying a chain of N uniform rods with the cart-pole's
+# constants per link, N = 1 .. 4, fused (K = 200) against unfused (K = 1).
+CHAIN_SWEEP = dict(name="chain-1M-200-Nsweep", n=1048576, T=200, K=[1, 200], N=[1, 2, 3, 4], seed=0)
+
 # Parity seeds: 0, 1, and one whose high 32 bits are nonzero.
 PARITY_SEEDS = (0, 1, (1 << 40) + 7)
 
 # Per env-step bytes of the trajectory: obs 4 x f32, action u8, reward f32, done u8.
 TRAJ_BYTES_PER_ENV_STEP = 4 * 4 + 1 + 4 + 1
+
+
+def chain_traj_bytes_per_env_step(n_links: int) -> int:
+    """Trajectory bytes per env-step of the chain: obs (2 N + 2) x f32, action
+    u8, reward f32, done u8."""
+    return 4 * (2 * n_links + 2) + 1 + 4 + 1
 
 
 def mlp_weights(seed: int, hidden: int = 64):
