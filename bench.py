@@ -347,7 +347,69 @@ def fusion_sweeps(stream) -> dict:
 
     out[workloads.WORKLOADS[workloads.MLP]["name"]] = policy_sweep(stream)
     out[workloads.C_SWEEP["name"]] = compute_factor_sweep(stream)
+    out[workloads.CHAIN_SWEEP["name"]] = chain_sweep(stream)
     return out
+
+
+def chain_flops_per_step(N: int) -> int:
+    """fp32 operations of one explicit-Euler iteration of the N-link chain, as
+    the definition lists them (a product, sum or division counts 1, an FMA 2),
+    on the common path where every link angle is within pi/4 (no reduction):
+    per link the sin/cos series (18) and phid^2; the mass matrix's cart row and
+    each link pair's cos(phi_j - phi_k) and coupling; the forces; the
+    elimination (a reciprocal per pivot, a multiplier and an FMA per updated
+    entry and right-hand side); the back substitution; the Euler update."""
+    pairs = N * (N - 1) // 2
+    flops = 18 * N + N                  # sin/cos series, phid^2
+    flops += N + 4 * pairs              # A_0k; per pair s s, fma, L h * cos
+    flops += 3 * N + N + 8 * pairs      # f_0 terms; g h s; per pair c s, fma, L h * sin, two fmas
+    S = N + 1
+    for p in range(S - 1):
+        flops += 1                      # 1 / A_pp
+        for i in range(p + 1, S):
+            flops += 1 + 2 * (S - i) + 2
+    flops += 1                          # 1 / A_NN
+    for i in range(S):
+        flops += 2 * (S - 1 - i) + 1    # back substitution
+    flops += 4 * S                      # Euler: 2 (N + 1) FMAs
+    return flops
+
+
+def chain_sweep(stream) -> dict:
+    """The second simulator: 1,048,576 envs x 200 steps of the N-link chain,
+    N = 1 .. 4, fused (one K = 200 launch) against unfused (200 launches of K =
+    1), with the fused launch against the HBM roofline (trajectory plus the
+    state once) and against the fp32 vector peak (the definition's operations
+    per env-step, chain_flops_per_step)."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.CHAIN_SWEEP
+    n, T = w["n"], w["T"]
+    rows = {}
+    for N in w["N"]:
+        sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream, links=N)
+        sim.reset(w["seed"])
+        traj = Trajectory(T, n, S=sim.S)
+        entry = {}
+        state_b = (4 * sim.S + 4) * n * 2
+        traj_b = n * T * workloads.chain_traj_bytes_per_env_step(N)
+        for K in w["K"]:
+            ms = _time_schedule(sim, traj, [K] * (T // K), stream, reps=3)
+            algo = traj_b + state_b * (T // K) + 16 * ((n + 255) // 256) * (T // K)
+            entry[f"K{K}"] = {"ms": ms, "env_steps_per_s": n * T / (ms * 1e-3),
+                              "algorithmic_GBs": algo / (ms * 1e-3) / 1e9}
+        fused = entry[f"K{T}"]
+        fused["hbm_frac"] = fused["algorithmic_GBs"] / HBM_PEAK_GBS
+        fused["flops_per_env_step"] = chain_flops_per_step(N)
+        fused["TFLOPs"] = n * T * chain_flops_per_step(N) / (fused["ms"] * 1e-3) / 1e12
+        fused["fp32_frac"] = fused["TFLOPs"] / (2 * VALU_LANE_OPS_PER_S / 1e12)
+        entry["fusion_speedup"] = entry["K1"]["ms"] / fused["ms"]
+        rows[f"N{N}"] = entry
+        del traj
+        sim.close()
+        print(f"[bench] chain N={N}: K1 {entry['K1']['ms']:.2f} ms, K{T} {fused['ms']:.3f} ms "
+              f"({fused['hbm_frac']:.2f} of HBM, {fused['fp32_frac']:.2f} of fp32), {entry['fusion_speedup']:.1f}x",
+              file=sys.stderr, flush=True)
+    return rows
 
 
 def stream_ceiling(words: int, achieved_gbs: float, stream) -> dict:
@@ -370,6 +432,63 @@ def stream_ceiling(words: int, achieved_gbs: float, stream) -> dict:
     gbs = words * 16 / (ms * 1e-3) / 1e9
     del s, a, b
     return {"ms": ms, "GBs": gbs, "frac_of_stream_ceiling": achieved_gbs / gbs}
+
+
+# iterations per launch of each instruction-rate probe kind (about 1-3 ms)
+ISSUE_ITERS = {"fma": 16384, "select_fma": 8192, "exp": 4096, "rcp": 4096, "mfma": 1024, "mixed": 1024, "mul": 16384}
+CUS = 256
+
+
+def _probe_ms(kind: str, waves: int, iters: int, out, stream, reps: int = 5) -> float:
+    import torch
+    from paper_2207_07736_amd.probe import probe_issue
+    blocks = CUS * waves
+    probe_issue(kind, blocks, iters, out, stream)
+    times = []
+    for _ in range(reps):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        probe_issue(kind, blocks, iters, out, stream)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        times.append(start.elapsed_time(stop))
+    times.sort()
+    return times[len(times) // 2]
+
+
+def issue_rates(stream) -> dict:
+    """The instruction rates the kernels' bounds rest on (rlsim_probe_issue),
+    with `waves` waves per SIMD (256 CUs x 4 SIMDs): wave64 v_fma_f32 as fp32
+    lane operations per second, and v_mul_f32 likewise; the per-lane padding update (a select and an
+    FMA per word) as word updates per second; v_exp_f32 and v_rcp_f32 as
+    lanes per second; fp32 MFMA as TFLOP/s; and one MFMA wave beside one FMA
+    wave on every SIMD against each alone (serialised if the mixed time is the
+    sum of the two)."""
+    import torch
+    out = torch.empty(CUS * 8 * 256, dtype=torch.float32, device="cuda")
+    res = {}
+    for kind, waves in (("fma", 1), ("fma", 2), ("fma", 4), ("fma", 8), ("mul", 8), ("select_fma", 2),
+                        ("select_fma", 8), ("exp", 8), ("rcp", 8)):
+        it = ISSUE_ITERS[kind]
+        ms = _probe_ms(kind, waves, it, out, stream)
+        lanes = CUS * waves * 256 * it * 8
+        res[f"{kind}_w{waves}"] = {"ms": ms, "per_s": lanes / (ms * 1e-3),
+                                   "unit": "word updates" if kind == "select_fma" else "lane ops"}
+    it = ISSUE_ITERS["mfma"]
+    for waves in (1, 2):
+        ms = _probe_ms("mfma", waves, it, out, stream)
+        flops = CUS * waves * 4 * it * 4 * (32 * 32 * 2 * 2)
+        res[f"mfma_f32_w{waves}"] = {"ms": ms, "TFLOPs": flops / (ms * 1e-3) / 1e12}
+    # one MFMA wave and one FMA wave per SIMD, against each alone at one wave per SIMD
+    mixed = _probe_ms("mixed", 2, it, out, stream)
+    fma_alone = _probe_ms("fma", 1, 16 * it, out, stream)
+    res["mfma_beside_fma"] = {"mixed_ms": mixed, "mfma_alone_ms": res["mfma_f32_w1"]["ms"], "fma_alone_ms": fma_alone,
+                              "mixed_over_sum": mixed / (res["mfma_f32_w1"]["ms"] + fma_alone),
+                              "mixed_over_max": mixed / max(res["mfma_f32_w1"]["ms"], fma_alone)}
+    del out
+    print("[bench] issue rates: " + ", ".join(f"{k} {v.get('per_s', v.get('TFLOPs', v.get('mixed_over_sum'))):.3g}"
+                                             for k, v in res.items()), file=sys.stderr, flush=True)
+    return res
 
 
 def compute_factor_sweep(stream) -> dict:
@@ -430,6 +549,10 @@ def sweep_only(which: str) -> int:
     torch.cuda.set_stream(stream)
     if which == "ksweep":
         rows = {workloads.WORKLOADS[workloads.K_SWEEP]["name"]: k_sweep(stream)}
+    elif which == "chain":
+        rows = {workloads.CHAIN_SWEEP["name"]: chain_sweep(stream)}
+    elif which == "issue":
+        rows = {"issue_rates": issue_rates(stream)}
     else:
         rows = {workloads.C_SWEEP["name"]: compute_factor_sweep(stream)}
     print(json.dumps(rows), flush=True)
@@ -523,6 +646,40 @@ def copy_for_calibration() -> None:
     dst.copy_(src)
     torch.cuda.synchronize()
     del src, dst
+
+
+def chain_only(N: int, steps: int, warmup: int, copy_calibration: bool = False) -> int:
+    """Timed K = 200 launches of the chain workload alone (for profiling):
+    1,048,576 envs x 200 steps of the N-link chain, trajectory recorded."""
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+    w = workloads.CHAIN_SWEEP
+    n, T = w["n"], w["T"]
+    stream = torch.cuda.current_stream()
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream, links=N)
+    sim.reset(w["seed"])
+    traj = Trajectory(T, n, S=sim.S)
+    rows = traj.rows(0, T)
+    for _ in range(warmup):
+        sim.step(T, rows)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        sim.step(T, rows)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    algo = n * T * workloads.chain_traj_bytes_per_env_step(N) + (4 * sim.S + 4) * n * 2 + 16 * ((n + 255) // 256)
+    print(json.dumps({"workload": w["name"], "N": N, "K": T, "ms_per_launch": ms,
+                      "env_steps_per_s": n * T / (ms * 1e-3), "algorithmic_bytes_per_launch": algo,
+                      "algorithmic_GBs": algo / (ms * 1e-3) / 1e9,
+                      "TFLOPs": n * T * chain_flops_per_step(N) / (ms * 1e-3) / 1e12}), flush=True)
+    del traj
+    sim.close()
+    if copy_calibration:
+        copy_for_calibration()
+    return 0
 
 
 def unfused_only(steps: int, warmup: int, copy_calibration: bool) -> int:
@@ -632,9 +789,11 @@ def main() -> int:
                     help="time only the headline workload as 200 launches of K = 1 (profiling)")
     ap.add_argument("--wide", type=int, metavar="D",
                     help="time only the state-size workload (262,144 envs, K = 500) with D padding words")
+    ap.add_argument("--chain", type=int, metavar="N",
+                    help="time only the chain workload (1,048,576 envs, K = 200) with N links")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM traffic summary from two rocprofv3 counter CSVs and exit")
-    ap.add_argument("--sweep-only", choices=("ksweep", "csweep"),
+    ap.add_argument("--sweep-only", choices=("ksweep", "csweep", "chain", "issue"),
                     help="run only the K sweep with its HIP-graph form (65,536 envs x 1,000 steps) or only "
                          "the compute-factor sweep, print its rows as JSON (profiling)")
     args = ap.parse_args()
@@ -645,6 +804,8 @@ def main() -> int:
         return policy_only(args.policy, args.steps, args.warmup)
     if args.wide:
         return wide_only(args.wide, args.steps, args.warmup, args.copy_calibration)
+    if args.chain:
+        return chain_only(args.chain, args.steps, args.warmup, args.copy_calibration)
     if args.unfused:
         return unfused_only(args.steps, args.warmup, args.copy_calibration)
 

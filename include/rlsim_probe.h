@@ -1,8 +1,8 @@
 /*
  * rlsim_probe.h -- C ABI of the measurement aids beside librlsim.so
  * (librlsim_probe.so): the store-only probe of the trajectory layout, a
- * read/write stream probe, and the error probe of the policy kernel's
- * elementwise functions.
+ * read/write stream probe, the error probe of the policy kernel's
+ * elementwise functions, and an instruction-rate probe.
  *
  * The fused simulator kernel's unavoidable work is writing the trajectory
  * (section "Simulator Kernel Fusion": fusion removes the state round trips,
@@ -66,6 +66,30 @@ int rlsim_probe_policy_math(uint32_t lo_bits, uint64_t count, uint32_t* out_max,
  * Errors: -1 if n4 == 0 or a pointer is NULL or not 16-byte aligned; -3 if the
  * launch fails. */
 int rlsim_probe_stream(uint64_t n4, float* s, const float* a, const float* b, void* stream);
+
+/* Instruction-rate probe: the throughputs that bound the kernels (section
+ * "Simulator Complexity": the compute factor and state size make the step
+ * compute-bound; "Future Work": simulation fused with MFMA inference).  One
+ * launch of `blocks` workgroups of 256 threads (four waves; 256 blocks put
+ * one wave on each SIMD of a 256-CU device, 256 w blocks w waves), each lane
+ * running `iters` iterations of eight independent chains (MFMA: four) of one
+ * instruction kind:
+ *   kind 0  v_fma_f32 x <- x * 1 + 1, x0 = lane + j       -> x0 + iters
+ *   kind 1  the per-lane padding update t <- u ? 1 : -0, s <- fma(1, s, t),
+ *           u = (lane + i) odd, s0 = j                     -> s0 + #odd steps
+ *   kind 2  v_exp_f32 x <- 2^-x                            -> the root of x = 2^-x
+ *   kind 3  v_rcp_f32 x <- 1 / x, x0 = 2^j                 -> x0 (even iters)
+ *   kind 4  v_mfma_f32_32x32x2_f32 C <- A B + C, A = B = 1 -> 2 iters per element
+ *   kind 5  kind 4 with `iters` and kind 0 with 16 iters (about as long) in
+ *           alternate waves (workgroup b, wave w: MFMA when b + w is even), so
+ *           that both share each SIMD
+ *   kind 6  v_mul_f32 x <- x * 1, x0 = lane + j            -> x0
+ * out (caller-owned DEVICE, blocks * 256 floats) receives per thread the sum
+ * of its chains' final values (kinds 0-3: over j = 0..7; MFMA: elements 0, 5,
+ * 10, 15 of the four accumulators, 8 iters).  The caller times the launch.
+ * Errors: -1 if kind > 6, blocks == 0 or > 2^20, iters == 0 or > 2^22 (kind
+ * 5: > 2^19), or out is NULL or not 4-byte aligned; -3 if the launch fails. */
+int rlsim_probe_issue(uint32_t kind, uint32_t blocks, uint32_t iters, float* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,11 +1,11 @@
-// k_wide.hip.h -- cart-pole with a wide padding state (D > 16 words per
+// k_wide.hip.h -- cart-pole with a wide padding state (D > 64 words per
 // environment, the state-size factor S of the paper's "Simulator Complexity"),
 // too many to keep in one thread's registers.  Each 512-step round runs the
 // cart-pole loop one thread per environment and records the action and done
 // bits in LDS (phase 1), then replays the padding recurrence from those bits
-// with the words spread over G lanes per environment (phase 2).  The padding
-// words only feed on (action, done), so the split is exact, and each word is
-// still read and written once per launch per round.
+// with each environment's words spread over the 64 lanes of a wave (phase 2).
+// The padding words only feed on (action, done), so the split is exact, and
+// each word is still read and written once per launch per round.
 #pragma once
 
 #include "k_cartpole.hip.h"
@@ -125,33 +125,191 @@ __device__ __forceinline__ void replay_uniform(float (&s)[W], const float (&pa)[
     }
 }
 
-// Phase 2: G lanes per environment, W words per lane (W a multiple of 4, held
-// as W / 4 float4 runs interleaved across the group's lanes).  Replays `steps`
-// steps from the LDS bits for the 64 / G environments a wave covers at a time,
-// for all of the wave's 64 envs.
-template <int G, int W>
+// The same replay for E environments at once (E = 2 or 4): each lane holds W
+// words of each of the E environments, and each step branches once on the E
+// action bits together (a binary tree of scalar bit tests down to one of 2^E
+// update paths, each E W in-place VALU updates), so the scalar work of a step
+// covers E W words per lane instead of W.  The done bits of the E environments
+// are tested together (their OR) and cleared out of line, each environment's
+// words only when its own bit is set.
+#define RM_FMA(e, i) "v_fma_f32 %[s" #e "_" #i "], %[a" #e "_" #i "], %[s" #e "_" #i "], %[b" #e "_" #i "]\n"
+#define RM_MUL(e, i) "v_mul_f32 %[s" #e "_" #i "], %[a" #e "_" #i "], %[s" #e "_" #i "]\n"
+#define RM_ZERO(e, i) "v_mov_b32 %[s" #e "_" #i "], 0\n"
+#define RM_R4(X, e) X(e, 0) X(e, 1) X(e, 2) X(e, 3)
+#define RM_R8(X, e) RM_R4(X, e) X(e, 4) X(e, 5) X(e, 6) X(e, 7)
+#define RM_R16(X, e) RM_R8(X, e) X(e, 8) X(e, 9) X(e, 10) X(e, 11) X(e, 12) X(e, 13) X(e, 14) X(e, 15)
+#define RM_ENV_1(R, e) R(RM_FMA, e)
+#define RM_ENV_0(R, e) R(RM_MUL, e)
+#define RM_CAT(a, b) a##b
+// leaf of the tree: environment e's words take the FMA path when bit e of the
+// leaf's code is set, the multiply path otherwise
+#define RM_LEAF2(R, b0, b1) RM_CAT(RM_ENV_, b0)(R, 0) RM_CAT(RM_ENV_, b1)(R, 1)
+#define RM_LEAF4(R, b0, b1, b2, b3) RM_LEAF2(R, b0, b1) RM_CAT(RM_ENV_, b2)(R, 2) RM_CAT(RM_ENV_, b3)(R, 3)
+#define RM_TEST(u, lab) "s_bitcmp1_b32 %[" #u "], %[c]\n s_cbranch_scc1 " #lab "%=\n"
+#define RM_TO_TAIL "s_branch Lm_tail%=\n"
+#define RM_CLEAR(R, e, d, next)                                  \
+    "s_bitcmp1_b32 %[" #d "], %[c]\n s_cbranch_scc0 " #next "%=\n" R(RM_ZERO, e) #next "%=:\n"
+#define RM_OUT_S(e, i) [s##e##_##i] "+v"(s##e[i]),
+#define RM_IN_A(e, i) [a##e##_##i] "v"(a##e[i]),
+#define RM_IN_B(e, i) [b##e##_##i] "v"(b##e[i]),
+#define RM_TAIL                                                  \
+    "Lm_tail%=:\n s_bitcmp1_b32 %[dor], %[c]\n s_cbranch_scc1 Lm_zero%=\n" \
+    "Lm_next%=:\n s_add_u32 %[c], %[c], 1\n s_cmp_lt_u32 %[c], %[m]\n"   \
+    "s_cbranch_scc1 Lm_step%=\n s_branch Lm_end%=\n"
+
+#define RM_REPLAY2(R)                                                                                     \
+    asm volatile("s_mov_b32 %[c], 0\n"                                                                    \
+                 "Lm_step%=:\n" RM_TEST(u1, Lm_1x) RM_TEST(u0, Lm_01) RM_LEAF2(R, 0, 0) RM_TO_TAIL        \
+                 "Lm_01%=:\n" RM_LEAF2(R, 1, 0) RM_TO_TAIL                                                 \
+                 "Lm_1x%=:\n" RM_TEST(u0, Lm_11) RM_LEAF2(R, 0, 1) RM_TO_TAIL                              \
+                 "Lm_11%=:\n" RM_LEAF2(R, 1, 1) RM_TAIL                                                    \
+                 "Lm_zero%=:\n" RM_CLEAR(R, 0, d0, Lm_z0) RM_CLEAR(R, 1, d1, Lm_z1)                        \
+                 "s_branch Lm_next%=\n"                                                                    \
+                 "Lm_end%=:\n"                                                                             \
+                 : R(RM_OUT_S, 0) R(RM_OUT_S, 1)[c] "=&s"(cnt)                                               \
+                 : R(RM_IN_A, 0) R(RM_IN_A, 1) R(RM_IN_B, 0) R(RM_IN_B, 1)[u0] "s"(u[0]), [u1] "s"(u[1]),   \
+                   [d0] "s"(d[0]), [d1] "s"(d[1]), [dor] "s"(dor), [m] "s"(m)                               \
+                 : "scc")
+
+#define RM_REPLAY4(R)                                                                                      \
+    asm volatile("s_mov_b32 %[c], 0\n"                                                                     \
+                 "Lm_step%=:\n" RM_TEST(u3, Lm_1xxx) RM_TEST(u2, Lm_01xx) RM_TEST(u1, Lm_001x)             \
+                 RM_TEST(u0, Lm_0001) RM_LEAF4(R, 0, 0, 0, 0) RM_TO_TAIL                                     \
+                 "Lm_0001%=:\n" RM_LEAF4(R, 1, 0, 0, 0) RM_TO_TAIL                                          \
+                 "Lm_001x%=:\n" RM_TEST(u0, Lm_0011) RM_LEAF4(R, 0, 1, 0, 0) RM_TO_TAIL                     \
+                 "Lm_0011%=:\n" RM_LEAF4(R, 1, 1, 0, 0) RM_TO_TAIL                                          \
+                 "Lm_01xx%=:\n" RM_TEST(u1, Lm_011x) RM_TEST(u0, Lm_0101) RM_LEAF4(R, 0, 0, 1, 0) RM_TO_TAIL \
+                 "Lm_0101%=:\n" RM_LEAF4(R, 1, 0, 1, 0) RM_TO_TAIL                                          \
+                 "Lm_011x%=:\n" RM_TEST(u0, Lm_0111) RM_LEAF4(R, 0, 1, 1, 0) RM_TO_TAIL                     \
+                 "Lm_0111%=:\n" RM_LEAF4(R, 1, 1, 1, 0) RM_TO_TAIL                                          \
+                 "Lm_1xxx%=:\n" RM_TEST(u2, Lm_11xx) RM_TEST(u1, Lm_101x) RM_TEST(u0, Lm_1001)             \
+                 RM_LEAF4(R, 0, 0, 0, 1) RM_TO_TAIL                                                          \
+                 "Lm_1001%=:\n" RM_LEAF4(R, 1, 0, 0, 1) RM_TO_TAIL                                          \
+                 "Lm_101x%=:\n" RM_TEST(u0, Lm_1011) RM_LEAF4(R, 0, 1, 0, 1) RM_TO_TAIL                     \
+                 "Lm_1011%=:\n" RM_LEAF4(R, 1, 1, 0, 1) RM_TO_TAIL                                          \
+                 "Lm_11xx%=:\n" RM_TEST(u1, Lm_111x) RM_TEST(u0, Lm_1101) RM_LEAF4(R, 0, 0, 1, 1) RM_TO_TAIL \
+                 "Lm_1101%=:\n" RM_LEAF4(R, 1, 0, 1, 1) RM_TO_TAIL                                          \
+                 "Lm_111x%=:\n" RM_TEST(u0, Lm_1111) RM_LEAF4(R, 0, 1, 1, 1) RM_TO_TAIL                     \
+                 "Lm_1111%=:\n" RM_LEAF4(R, 1, 1, 1, 1) RM_TAIL                                             \
+                 "Lm_zero%=:\n" RM_CLEAR(R, 0, d0, Lm_z0) RM_CLEAR(R, 1, d1, Lm_z1)                         \
+                 RM_CLEAR(R, 2, d2, Lm_z2) RM_CLEAR(R, 3, d3, Lm_z3)                                         \
+                 "s_branch Lm_next%=\n"                                                                     \
+                 "Lm_end%=:\n"                                                                              \
+                 : R(RM_OUT_S, 0) R(RM_OUT_S, 1) R(RM_OUT_S, 2) R(RM_OUT_S, 3)[c] "=&s"(cnt)                  \
+                 : R(RM_IN_A, 0) R(RM_IN_A, 1) R(RM_IN_A, 2) R(RM_IN_A, 3) R(RM_IN_B, 0) R(RM_IN_B, 1)        \
+                   R(RM_IN_B, 2) R(RM_IN_B, 3)[u0] "s"(u[0]), [u1] "s"(u[1]), [u2] "s"(u[2]), [u3] "s"(u[3]), \
+                   [d0] "s"(d[0]), [d1] "s"(d[1]), [d2] "s"(d[2]), [d3] "s"(d[3]), [dor] "s"(dor), [m] "s"(m) \
+                 : "scc")
+
+// Steps 0 .. m-1 (1 <= m <= 32) of one 32-step bit word for E environments:
+// u[e], d[e] their action and done bits (wave-uniform), s/a/b the lane's W
+// words of each.
+template <int E, int W>
+__device__ __forceinline__ void replay_multi(float (&s0)[W], float (&s1)[W], float (&s2)[W], float (&s3)[W],
+                                             const float (&a0)[W], const float (&a1)[W], const float (&a2)[W],
+                                             const float (&a3)[W], const float (&b0)[W], const float (&b1)[W],
+                                             const float (&b2)[W], const float (&b3)[W], const uint32_t (&u)[4],
+                                             const uint32_t (&d)[4], uint32_t m)
+{
+    uint32_t cnt;
+    const uint32_t dor = d[0] | d[1] | d[2] | d[3];
+    if constexpr (E == 4 && W == 8) RM_REPLAY4(RM_R8);
+    else if constexpr (E == 4 && W == 4) RM_REPLAY4(RM_R4);
+    else if constexpr (E == 2 && W == 16) RM_REPLAY2(RM_R16);
+    else if constexpr (E == 2 && W == 8) RM_REPLAY2(RM_R8);
+    else if constexpr (E == 2 && W == 4) RM_REPLAY2(RM_R4);
+    else static_assert(E == 0, "no replay for this (E, W)");
+    (void)s2; (void)s3; (void)a2; (void)a3; (void)b2; (void)b3;
+}
+
+// Phase 2 with E environments replayed together: W words per lane per
+// environment, loaded as float4 with the placement of replay_padding, for the
+// 64 environments of the wave, E at a time.
+template <int W, int E>
+__device__ __forceinline__ void replay_padding_multi(const StepArgs& a, const uint32_t* lds_u, const uint32_t* lds_d,
+                                                     uint32_t steps, uint32_t blk)
+{
+    static_assert(W % 4 == 0 && (E == 2 || E == 4), "bad multi-environment replay shape");
+    const uint32_t lane = threadIdx.x % 64u, wave = threadIdx.x / 64u;
+    const uint32_t chunk_words = 64u * W;
+    const uint32_t n_chunks = (a.Dp + chunk_words - 1u) / chunk_words;
+    for (uint32_t pass = 0; pass < 64u / E; ++pass) {
+        uint32_t col[4], env[4];
+        bool live[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            col[e] = wave * 64u + pass * E + (uint32_t)(e < E ? e : 0);
+            env[e] = blk * kBlock + col[e];
+            live[e] = e < E && env[e] < a.n;
+        }
+        for (uint32_t c = 0; c < n_chunks; ++c) {
+            const uint32_t base = c * chunk_words + 4u * lane;
+            float s[4][W], pa[4][W], pb[4][W];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const size_t row = (size_t)env[e] * a.Dp;
+#pragma unroll
+                for (int i = 0; i < W; i += 4) {
+                    const uint32_t j = base + (uint32_t)(i / 4) * 256u;
+                    const bool on = live[e] && j < a.Dp;
+                    const float4 vs = on ? *reinterpret_cast<const float4*>(a.pad_s + row + j) : float4{0, 0, 0, 0};
+                    const float4 va = on ? *reinterpret_cast<const float4*>(a.pad_a + row + j) : float4{0, 0, 0, 0};
+                    const float4 vb = on ? *reinterpret_cast<const float4*>(a.pad_b + row + j) : float4{0, 0, 0, 0};
+                    s[e][i] = vs.x; s[e][i + 1] = vs.y; s[e][i + 2] = vs.z; s[e][i + 3] = vs.w;
+                    pa[e][i] = va.x; pa[e][i + 1] = va.y; pa[e][i + 2] = va.z; pa[e][i + 3] = va.w;
+                    pb[e][i] = vb.x; pb[e][i + 1] = vb.y; pb[e][i + 2] = vb.z; pb[e][i + 3] = vb.w;
+                }
+            }
+            for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
+                uint32_t ub[4], db[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    ub[e] = e < E ? __builtin_amdgcn_readfirstlane(lds_u[w32 * kBlock + col[e]]) : 0u;
+                    db[e] = e < E ? __builtin_amdgcn_readfirstlane(lds_d[w32 * kBlock + col[e]]) : 0u;
+                }
+                const uint32_t m = __builtin_amdgcn_readfirstlane(min(32u, steps - w32 * 32u));
+                replay_multi<E, W>(s[0], s[1], s[2], s[3], pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3],
+                                   ub, db, m);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const size_t row = (size_t)env[e] * a.Dp;
+#pragma unroll
+                for (int i = 0; i < W; i += 4) {
+                    const uint32_t j = base + (uint32_t)(i / 4) * 256u;
+                    if (live[e] && j < a.Dp)
+                        *reinterpret_cast<float4*>(a.pad_s + row + j) =
+                            float4{s[e][i], s[e][i + 1], s[e][i + 2], s[e][i + 3]};
+                }
+            }
+        }
+    }
+}
+
+// Phase 2, one environment per wave at a time: the lane holds W words (W a
+// multiple of 4, as W / 4 float4 runs: float4 q of lane l holds words
+// 4 l + 256 q .. +3 of a 64 W-word chunk, so each float4 load and store of the
+// wave covers 1 KB contiguously), and the bits are wave-uniform, so each step
+// is a scalar branch and one FMA or multiply per word.
+template <int W>
 __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t* lds_u, const uint32_t* lds_d,
                                                uint32_t steps, uint32_t blk)
 {
-    static_assert(W % 4 == 0 && 64 % G == 0, "bad wide-padding shape");
+    static_assert(W % 4 == 0, "bad wide-padding shape");
     const uint32_t lane = threadIdx.x % 64u, wave = threadIdx.x / 64u;
-    const uint32_t gi = lane / G, gl = lane % G;            // env slot in the wave, lane in its group
-    const uint32_t chunk_words = (uint32_t)(G * W);
+    const uint32_t chunk_words = 64u * W;
     const uint32_t n_chunks = (a.Dp + chunk_words - 1u) / chunk_words;
-    // a pass covers 64 / G environments, so the wave's 64 take G passes
-    for (uint32_t pass = 0; pass < (uint32_t)G; ++pass) {
-        const uint32_t col = wave * 64u + pass * (64u / G) + gi;   // env column in the block
+    for (uint32_t pass = 0; pass < 64u; ++pass) {
+        const uint32_t col = wave * 64u + pass;      // env column in the block
         const uint32_t env = blk * kBlock + col;
         const bool live = env < a.n;
         for (uint32_t c = 0; c < n_chunks; ++c) {
-            // float4 q of this lane holds words base + q * 4G .. +3: the G lanes of
-            // a group read and write 16 G contiguous bytes per instruction
-            const uint32_t base = c * chunk_words + 4u * gl;
+            const uint32_t base = c * chunk_words + 4u * lane;
             float s[W], pa[W], pb[W];
             const size_t row = (size_t)env * a.Dp;
 #pragma unroll
             for (int i = 0; i < W; i += 4) {
-                const uint32_t j = base + (uint32_t)(i / 4) * (4u * G);
+                const uint32_t j = base + (uint32_t)(i / 4) * 256u;
                 const bool on = live && j < a.Dp;
                 const float4 vs = on ? *reinterpret_cast<const float4*>(a.pad_s + row + j) : float4{0, 0, 0, 0};
                 const float4 va = on ? *reinterpret_cast<const float4*>(a.pad_a + row + j) : float4{0, 0, 0, 0};
@@ -161,32 +319,15 @@ __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t
                 pb[i] = vb.x; pb[i + 1] = vb.y; pb[i + 2] = vb.z; pb[i + 3] = vb.w;
             }
             for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
-                uint32_t ub = lds_u[w32 * kBlock + col];
-                uint32_t db = lds_d[w32 * kBlock + col];
+                const uint32_t ub = lds_u[w32 * kBlock + col];
+                const uint32_t db = lds_d[w32 * kBlock + col];
                 const uint32_t m = min(32u, steps - w32 * 32u);
-                if (G == 64) {
-                    // one environment per wave: the bits are wave-uniform, so
-                    // each step is a scalar branch and one FMA per word
-                    replay_uniform<W>(s, pa, pb, __builtin_amdgcn_readfirstlane(ub), __builtin_amdgcn_readfirstlane(db),
-                                      __builtin_amdgcn_readfirstlane(m));
-                } else {
-                    for (uint32_t i = 0; i < m; ++i) {
-                        const bool u = (ub >> i) & 1u;
-                        const bool d = (db >> i) & 1u;
-#pragma unroll
-                        for (int j = 0; j < W; ++j) s[j] = pad_update(pa[j], s[j], pb[j], u);
-                        // episode ends are rare: clear words only in a wave that has one
-                        if (__builtin_amdgcn_ballot_w64(d) != 0u) {
-                            asm volatile("" ::: "memory");
-#pragma unroll
-                            for (int j = 0; j < W; ++j) s[j] = d ? 0.0f : s[j];
-                        }
-                    }
-                }
+                replay_uniform<W>(s, pa, pb, __builtin_amdgcn_readfirstlane(ub), __builtin_amdgcn_readfirstlane(db),
+                                  __builtin_amdgcn_readfirstlane(m));
             }
 #pragma unroll
             for (int i = 0; i < W; i += 4) {
-                const uint32_t j = base + (uint32_t)(i / 4) * (4u * G);
+                const uint32_t j = base + (uint32_t)(i / 4) * 256u;
                 if (live && j < a.Dp)
                     *reinterpret_cast<float4*>(a.pad_s + row + j) = float4{s[i], s[i + 1], s[i + 2], s[i + 3]};
             }
@@ -194,7 +335,7 @@ __device__ __forceinline__ void replay_padding(const StepArgs& a, const uint32_t
     }
 }
 
-template <int G, int W, bool REC, bool STATS>
+template <int W, bool REC, bool STATS, int E = 1>
 __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
 {
     __shared__ uint32_t lds_u[kChunkWords * kBlock];
@@ -215,7 +356,8 @@ __global__ __launch_bounds__(kBlock) void k_cartpole_wide(StepArgs a)
             rec.flush();
         }
         __syncthreads();
-        replay_padding<G, W>(a, lds_u, lds_d, steps, blk);
+        if constexpr (E > 1) replay_padding_multi<W, E>(a, lds_u, lds_d, steps, blk);
+        else replay_padding<W>(a, lds_u, lds_d, steps, blk);
         __syncthreads();
     }
     if (live) core.store(a);

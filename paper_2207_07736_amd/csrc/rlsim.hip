@@ -202,8 +202,11 @@ bool aligned4(const void* ptr) { return ((uintptr_t)ptr & 3u) == 0u; }
 unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 
 // Largest padding count of the register-resident (one thread per env) kernel;
-// above it the two-phase wide kernel holds the words.
-constexpr uint32_t kMaxRegisterWords = 16u;
+// above it the two-phase wide kernel holds the words.  (262,144 envs x 500
+// steps: D = 64 1.23 ms with the 64 words in each thread's registers, 250
+// VGPRs, against 1.37 ms for the two-phase kernel replaying them on 8 lanes
+// per environment; D = 32 0.85 against 1.08 ms.)
+constexpr uint32_t kMaxRegisterWords = 64u;
 // Fewest steps per call for which a trajectory-recording call runs the
 // warp-specialised kernel: without padding words, and with 1-4 padding words.
 // Below them the hand-over's pipeline fill and drain cost more than the faster
@@ -229,18 +232,21 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
         else if (a.D == 0u) hipLaunchKernelGGL((k_cartpole_fused<0, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 16u) hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 32u) hipLaunchKernelGGL((k_cartpole_fused<32, REC, STATS>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_fused<64, REC, STATS>), grid, block, 0, s, a);
     } else {
-        // lanes per env x words per lane: 8 x 4 for up to 32 words and 8 x 8 for
-        // up to 64 (per-lane bits, 8 envs per wave; a lane replays all W of its
-        // words, so W follows D); otherwise one env per wave with uniform bits
-        if (a.D <= 32u) hipLaunchKernelGGL((k_cartpole_wide<8, 4, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<8, 8, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<64, 4, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<64, 8, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<64, 16, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<64, 32, REC, STATS>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_cartpole_wide<64, 64, REC, STATS>), grid, block, 0, s, a);
+        // one environment per wave in the replay (wave-uniform bits), W words
+        // per lane; E environments replayed together where that pays
+        // (262,144 envs x 500 steps: D = 256 1.84 / 1.98 / 2.24 ms for E = 4 / 2
+        // / 1, D = 512 3.10 / 2.55 / 2.81 ms, D = 1,024 E = 2 5.0 against E = 1
+        // 3.94 ms: four environments of 8 words, or two of 16, take the
+        // kernel past 128 VGPRs and below four waves per SIMD)
+        if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, REC, STATS, 4>), grid, block, 0, s, a);
+        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, REC, STATS, 2>), grid, block, 0, s, a);
+        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, REC, STATS>), grid, block, 0, s, a);
+        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, REC, STATS>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_wide<64, REC, STATS>), grid, block, 0, s, a);
     }
     return hipGetLastError();
 }

@@ -5,9 +5,10 @@
 // planes first: of the orders measured for these planes this one writes
 // fastest (about 6 % faster than the same stores with other instructions
 // between them), so the probe's time is the ceiling for the layout.  The
-// policy-math error probe (math_probe.hip.h) and the read/write stream probe
-// (stream_probe.hip.h) are included at the end (one translation unit: the
-// kernel headers define kernels).
+// policy-math error probe (math_probe.hip.h), the read/write stream probe
+// (stream_probe.hip.h) and the instruction-rate probes (issue_probe.hip.h) are
+// included at the end (one translation unit: the kernel headers define
+// kernels).
 #include <hip/hip_runtime.h>
 
 #include "rlsim_probe.h"
@@ -60,5 +61,6 @@ extern "C" int rlsim_probe_store(uint32_t n, uint32_t K, float* obs, uint8_t* ac
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
+#include "issue_probe.hip.h"
 #include "math_probe.hip.h"
 #include "stream_probe.hip.h"

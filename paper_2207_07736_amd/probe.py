@@ -1,6 +1,7 @@
 """Thin ctypes binding of librlsim_probe.so (include/rlsim_probe.h): the
-store-only probe of the trajectory layout, a read/write stream probe and the
-error probe of the policy kernel's elementwise functions, measurement aids.  Argument
+store-only probe of the trajectory layout, a read/write stream probe, the
+error probe of the policy kernel's elementwise functions and the
+instruction-rate probe, measurement aids.  Argument
 marshalling only; fails loudly if the library has not been built."""
 from __future__ import annotations
 
@@ -9,7 +10,8 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
-PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream")
+PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream", "rlsim_probe_issue")
+ISSUE_KINDS = ("fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul")
 
 
 def _load():
@@ -23,6 +25,8 @@ def _load():
     L.rlsim_probe_policy_math.restype = ctypes.c_int
     L.rlsim_probe_stream.argtypes = [ctypes.c_uint64, vp, vp, vp, vp]
     L.rlsim_probe_stream.restype = ctypes.c_int
+    L.rlsim_probe_issue.argtypes = [u32, u32, u32, vp, vp]
+    L.rlsim_probe_issue.restype = ctypes.c_int
     return L
 
 
@@ -61,3 +65,16 @@ def probe_stream(s, a, b, stream=None) -> None:
     rc = probe_lib.rlsim_probe_stream(s.numel() // 4, _ptr(s), _ptr(a), _ptr(b), st)
     if rc != 0:
         raise ValueError(f"rlsim_probe_stream rejected its arguments (status {rc})")
+
+
+def probe_issue(kind: str, blocks: int, iters: int, out, stream=None) -> None:
+    """Run the instruction-rate probe `kind` (one of ISSUE_KINDS) over `blocks`
+    workgroups of 256 threads, `iters` iterations each, results into out (a
+    float32 device tensor of blocks * 256); raises ValueError on a rejected
+    argument."""
+    if out.numel() < blocks * 256:
+        raise ValueError("out must hold blocks * 256 floats")
+    st = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    rc = probe_lib.rlsim_probe_issue(ISSUE_KINDS.index(kind), int(blocks), int(iters), _ptr(out), st)
+    if rc != 0:
+        raise ValueError(f"rlsim_probe_issue rejected its arguments (status {rc})")

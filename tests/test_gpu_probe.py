@@ -74,3 +74,57 @@ def test_stream_probe_values():
     torch.cuda.synchronize()
     assert np.array_equal(ts.cpu().numpy().view(np.uint32), want.view(np.uint32))
     assert np.array_equal(ta.cpu().numpy(), a) and np.array_equal(tb.cpu().numpy(), b)
+
+
+@pytest.mark.parametrize("kind", ["fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul"])
+def test_issue_probe_values(kind):
+    """rlsim_probe_issue runs the instruction chains it claims: every thread's
+    sum of chain results equals the closed form of its kind (exact integers for
+    the FMA, select and MFMA chains and the rcp cycle; the fixed point of
+    x = 2^-x for exp, to the hardware exp2's accuracy)."""
+    import math
+
+    import numpy as np
+    from paper_2207_07736_amd.probe import probe_issue
+    blocks, iters = 3, 101
+    out = torch.full((blocks * 256,), float("nan"), dtype=torch.float32, device="cuda")
+    probe_issue(kind, blocks, iters, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().reshape(blocks, 4, 64)
+    lane = np.arange(64)
+    fma = np.sum([lane + j + iters for j in range(8)], axis=0).astype(np.float64)
+    if kind == "fma":
+        want = np.broadcast_to(fma, got.shape)
+    elif kind == "mul":
+        want = np.broadcast_to(np.sum([lane + j for j in range(8)], axis=0).astype(np.float64), got.shape)
+    elif kind == "select_fma":
+        odd_steps = np.where(lane % 2 == 0, iters // 2, (iters + 1) // 2)
+        want = np.broadcast_to(np.sum([j + odd_steps for j in range(8)], axis=0), got.shape)
+    elif kind == "rcp":
+        want = np.full(got.shape, sum(2.0**-j for j in range(8)))          # odd iteration count: reciprocals
+    elif kind == "mfma":
+        want = np.full(got.shape, 8.0 * iters)
+    elif kind == "mixed":
+        b = np.arange(blocks)[:, None, None]
+        w = np.arange(4)[None, :, None]
+        fma16 = np.sum([lane + j + 16 * iters for j in range(8)], axis=0)
+        want = np.where((b + w) % 2 == 1, fma16[None, None, :], 8.0 * iters)
+    else:
+        root = 0.5
+        for _ in range(200):
+            root = 2.0 ** -root
+        assert abs(root - 0.6411857445) < 1e-9
+        assert np.all(np.abs(got - 8 * root) < 8 * 2e-6), got.min()
+        return
+    assert np.array_equal(got.astype(np.float64), want), (kind, got[0, 0, :4], np.asarray(want)[0, 0, :4])
+    assert not math.isnan(float(got.sum()))
+
+
+def test_issue_probe_rejects_bad_arguments():
+    from paper_2207_07736_amd.probe import probe_issue
+    out = torch.zeros(256, dtype=torch.float32, device="cuda")
+    for kind, blocks, iters in (("fma", 0, 1), ("fma", 1, 0), ("mixed", 1, (1 << 19) + 1), ("fma", 1, (1 << 22) + 1)):
+        with pytest.raises(ValueError):
+            probe_issue(kind, blocks, iters, out)
+    with pytest.raises(ValueError):
+        probe_issue("fma", 2, 1, out)                                        # out too small
