@@ -98,6 +98,16 @@ def assert_bit_equal(gpu, ref, keys=("obs", "action", "reward", "done", "state",
 # enclosure still shows
 F32_P0_GATE = 1e-5
 
+# bf16 policy: fixed gates on the distribution of |p0_gpu - p0_oracle| over the
+# full-size check (8.4 M env-steps), beside the per-observation enclosure, so
+# that a systematic error smaller than the enclosure (8.2e-5 wide on average)
+# but larger than the observed spread still fails: mean <= 2e-6 (observed
+# 4.4e-7) and 99.99th percentile <= 1e-3 (observed 3.0e-4; the largest single
+# difference, 1.01e-3, is a hidden unit's bf16 rounding flip, inside its
+# enclosure).
+BF16_P0_MEAN_GATE = 2e-6
+BF16_P0_Q9999_GATE = 1e-3
+
 
 def policy_weights(seed, bias_scale=0.0):
     """The policy workload's weights from `seed`, with biases drawn at

@@ -110,7 +110,7 @@ def test_headline_launch_every_env_every_step():
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_policy_workload_32k_envs_every_step(dtype):
     import policy_bounds
-    from gpu_helpers import F32_P0_GATE, device_policy
+    from gpu_helpers import BF16_P0_MEAN_GATE, BF16_P0_Q9999_GATE, F32_P0_GATE, device_policy
 
     from paper_2207_07736_amd import Simulator, Trajectory
     w = workloads.WORKLOADS[workloads.MLP]
@@ -138,15 +138,19 @@ def test_policy_workload_32k_envs_every_step(dtype):
     pol = oracle.Policy(**wts, bf16=(dtype == "bf16"))
     errs = policy_bounds.errs()
 
+    dp0 = np.zeros((T, 4 * S), dtype=np.float32)          # |p0 - oracle p0| of every checked env-step
+
     def one(a, b):
         # each column range lies inside one slice of consecutive env ids
         if a == b:
             return None
         assert env_ids[b - 1] - env_ids[a] == b - 1 - a
         c = {key: v[..., a:b] for key, v in cols.items()}
+        part = np.zeros((T, b - a), dtype=np.float32)
         bad, first, stats = oracle.check_policy_rows(
             params, pol, seed, int(env_ids[a]), 0, c["obs"], c["action"], c["reward"], c["done"], c["policy_p0"],
-            errs, logp=c["logp"], value=c["value"])
+            errs, logp=c["logp"], value=c["value"], dp0_out=part)
+        dp0[:, a:b] = part
         stats["width_sum"] = stats["mean_width"] * (b - a) * T
         return bad, (None if first is None else (first[0], int(env_ids[a + first[1]]))), stats
 
@@ -163,7 +167,9 @@ def test_policy_workload_32k_envs_every_step(dtype):
     exempt = sum(r[2]["exempt"] for r in res)
     max_width = max(r[2]["max_width"] for r in res)
     mean_width = sum(r[2]["width_sum"] for r in res) / (4 * S * T)
-    print(f"{dtype}: worst |p0 - oracle| {worst:.3g}, p0 enclosure width mean {mean_width:.3g} max {max_width:.3g}, "
+    mean_dp0, p9999 = float(dp0.astype(np.float64).mean()), float(np.quantile(dp0, 0.9999))
+    print(f"{dtype}: worst |p0 - oracle| {worst:.3g}, mean {mean_dp0:.3g}, 99.99th percentile {p9999:.3g}, "
+          f"p0 enclosure width mean {mean_width:.3g} max {max_width:.3g}, "
           f"{exempt} actions differ from the oracle's", flush=True)
     if bad:
         k, env = firsts[0]
@@ -179,6 +185,8 @@ def test_policy_workload_32k_envs_every_step(dtype):
     assert exempt <= 4 * S * T // 10000, exempt
     if dtype == "f32":
         assert worst <= F32_P0_GATE, worst
+    else:
+        assert mean_dp0 <= BF16_P0_MEAN_GATE and p9999 <= BF16_P0_Q9999_GATE, (mean_dp0, p9999)
     assert int(cols["done"].astype(bool).sum()) > 0
 
 
