@@ -636,6 +636,48 @@ def wide_only(D: int, steps: int, warmup: int, copy_calibration: bool = False) -
     return 0
 
 
+def store_ceiling_only(steps: int) -> int:
+    """The headline's store ceiling against a plain fill (for counters): the
+    store-only probe writing the 4,194,304-env x 200-row trajectory (seven
+    planes per row, byte planes first), then torch's fill of one contiguous
+    buffer of the same 18.45 GB, then the headline launch itself, each `steps`
+    times, with the per-launch times printed."""
+    import torch
+    from paper_2207_07736_amd import Simulator, Trajectory
+    from paper_2207_07736_amd.probe import probe_store
+    w = workloads.WORKLOADS[workloads.HEADLINE]
+    n, T = w["n"], w["T"]
+    stream = torch.cuda.current_stream()
+    traj = Trajectory(T, n)
+    out = {}
+
+    def timed(name, fn):
+        fn()
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for _ in range(steps):
+            fn()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        out[name] = start.elapsed_time(stop) / steps
+
+    timed("store_probe_ms", lambda: probe_store(n, T, traj.obs, traj.action, traj.reward, traj.done, stream))
+    flat = torch.empty(n * T * workloads.TRAJ_BYTES_PER_ENV_STEP // 4, dtype=torch.float32, device="cuda")
+    timed("plain_fill_ms", lambda: flat.fill_(1.0))
+    del flat
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
+    sim.reset(w["seed"])
+    rows = traj.rows(0, T)
+    timed("headline_ms", lambda: sim.step(T, rows))
+    sim.close()
+    del traj
+    b = n * T * workloads.TRAJ_BYTES_PER_ENV_STEP
+    out.update({k.replace("_ms", "_TBs"): b / (v * 1e-3) / 1e12 for k, v in list(out.items())})
+    print(json.dumps({"workload": w["name"], "bytes": b, **out}), flush=True)
+    return 0
+
+
 def copy_for_calibration() -> None:
     """One plain device copy of COPY_BYTES: what the HBM byte counters read for
     it scales their readings of the kernels."""
@@ -789,6 +831,9 @@ def main() -> int:
                     help="time only the headline workload as 200 launches of K = 1 (profiling)")
     ap.add_argument("--wide", type=int, metavar="D",
                     help="time only the state-size workload (262,144 envs, K = 500) with D padding words")
+    ap.add_argument("--store-ceiling", action="store_true",
+                    help="time the headline's store-only probe, a plain fill of the same bytes and the headline "
+                         "launch (for counters)")
     ap.add_argument("--chain", type=int, metavar="N",
                     help="time only the chain workload (1,048,576 envs, K = 200) with N links")
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -806,6 +851,8 @@ def main() -> int:
         return wide_only(args.wide, args.steps, args.warmup, args.copy_calibration)
     if args.chain:
         return chain_only(args.chain, args.steps, args.warmup, args.copy_calibration)
+    if args.store_ceiling:
+        return store_ceiling_only(args.steps)
     if args.unfused:
         return unfused_only(args.steps, args.warmup, args.copy_calibration)
 
