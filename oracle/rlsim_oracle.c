@@ -262,7 +262,9 @@ int orc_terminated(const orc_params* p, const float s[4])
 /* Initial state of an episode that begins at global step t: stream RESET,  */
 /* counter block t/8, words 0..3 -> x, xd, th, thd.  Episodes of one env    */
 /* that begin in the same 8-step block would share a draw; with the default  */
-/* constants every episode lasts at least 8 steps, so none do.               */
+/* constants every episode lasts at least 8 steps (shown for the whole reset */
+/* box and every action sequence by interval arithmetic over the fp32 step,  */
+/* tests/test_oracle_episode_bound.py), so none do.                          */
 void orc_reset_draw(const orc_params* p, uint64_t seed, uint32_t env, uint32_t t, float out[4])
 {
     uint32_t w[4];
