@@ -512,3 +512,41 @@ def test_step_rejects_rows_cut_for_another_call():
         del tr, other_n, other_s
     finally:
         sim.close()
+
+
+@pytest.mark.parametrize("n", [4, 260, 1028, 4096])
+def test_warp_specialised_more_shapes(n):
+    """The warp-specialised kernel at environment counts that are multiples of
+    4 (a full block, a few lanes of a second one), over chunk tails (K = 17, 18,
+    19, 65) and long calls."""
+    sched = [16, 17, 18, 19, 65, 200]
+    T = sum(sched)
+    g = gpu_run(n, T, sched, seed=21)
+    r = oracle_run(n, T, sched, seed=21)
+    assert_bit_equal(g, r)
+    _stats_equal(g["stats"], r["stats"])
+
+
+def test_warp_specialised_planes_only_4_byte_aligned():
+    """Trajectory planes that are 4- but not 16-byte aligned (a buffer offset by
+    one float, which the ABI allows) record the oracle's trajectory bit for
+    bit."""
+    from paper_2207_07736_amd import Simulator, TrajRows, traj_struct
+    n, K = 1024, 40
+    sim = Simulator(n, 0, workloads.CARTPOLE)
+    try:
+        sim.reset(3)
+        obs_buf = torch.empty(K * 4 * n + 1, dtype=torch.float32, device="cuda")
+        rew_buf = torch.empty(K * n + 1, dtype=torch.float32, device="cuda")
+        obs, rew = obs_buf[1:].view(K, 4, n), rew_buf[1:].view(K, n)
+        act = torch.empty((K, n), dtype=torch.uint8, device="cuda")
+        done = torch.empty((K, n), dtype=torch.uint8, device="cuda")
+        assert obs.data_ptr() % 16 != 0
+        sim.step(K, TrajRows(traj_struct(obs, act, rew, done), K, n, 4))
+        torch.cuda.synchronize()
+        r = oracle_run(n, K, [K], seed=3)
+        assert np.array_equal(obs.cpu().numpy().view(np.uint32), r["obs"].view(np.uint32))
+        assert np.array_equal(act.cpu().numpy(), r["action"]) and np.array_equal(done.cpu().numpy(), r["done"])
+        assert bool((rew == 1.0).all())
+    finally:
+        sim.close()
