@@ -168,6 +168,13 @@ __device__ __forceinline__ void chain_reset_draw(const DevParams& p, uint32_t gi
     }
 }
 
+// ChainCore hook that does nothing (the rows, if any, are stored by the core).
+template <int N>
+struct ChainNoHook {
+    __device__ __forceinline__ void record(const ChainState<N>&, uint32_t, uint32_t) {}
+    __device__ __forceinline__ void advance() {}
+};
+
 // One environment's chain state and RNG words, advanced step by step: the
 // cart-pole's CartCore loop with the chain's state, step and reset draw.
 template <int N, bool REC, bool STATS>
@@ -198,7 +205,10 @@ struct ChainCore {
         abits = pick_word(aw, (t >> 5) & 3u);
     }
 
-    __device__ __forceinline__ void step()
+    // One step; hook.record(state, action, done byte) sees the row this step
+    // records, and hook.advance() runs after the step is complete.
+    template <class Hook>
+    __device__ __forceinline__ void step(Hook& hook)
     {
         const uint32_t act = abits & 1u;
         abits >>= 1;
@@ -224,6 +234,7 @@ struct ChainCore {
             rew_row += plane;
             done_row += plane;
         }
+        hook.record(s, act, d);
         const bool reset = term || trunc;
 #pragma unroll
         for (int j = 0; j <= N; ++j) {
@@ -236,11 +247,13 @@ struct ChainCore {
             n_term += term ? 1u : 0u;
             n_trunc += trunc ? 1u : 0u;
         }
+        hook.advance();
     }
 
     // Steps t0 .. t0+K-1 in bodies of the eight steps that share one reset
     // block, as CartCore::run.
-    __device__ __forceinline__ void run(uint32_t t0, uint32_t K)
+    template <class Hook>
+    __device__ __forceinline__ void run(uint32_t t0, uint32_t K, Hook& hook)
     {
         uint32_t t = t0, k = 0;
         aw = philox(gid, t >> 7, STREAM_ACTION, c.p.key0, c.p.key1);
@@ -248,25 +261,25 @@ struct ChainCore {
         if (((t + 1u) & 7u) != 0u) {
             chain_reset_draw<N>(c.p, gid, (t + 1u) >> 3, rs);
             while (k < K && ((t + 1u) & 7u) != 0u) {
-                step();
+                step(hook);
                 ++t;
                 ++k;
             }
         }
         for (; K - k >= 8u; k += 8u, t += 8u) {
             chain_reset_draw<N>(c.p, gid, (t + 1u) >> 3, rs);
-            step();
+            step(hook);
             if (((t + 1u) & 31u) == 0u) refresh_actions(t + 1u);
 #pragma unroll 1
-            for (int i = 0; i < 7; ++i) step();
+            for (int i = 0; i < 7; ++i) step(hook);
         }
         if (k < K) {
             chain_reset_draw<N>(c.p, gid, (t + 1u) >> 3, rs);
-            step();
+            step(hook);
             ++t;
             ++k;
             if (k < K && (t & 31u) == 0u) refresh_actions(t);
-            for (; k < K; ++k) step();
+            for (; k < K; ++k) step(hook);
         }
     }
 
@@ -309,13 +322,126 @@ __global__ __launch_bounds__(kBlock) void k_chain_fused(ChainArgs a)
             core.rew_row = a.reward;
             core.done_row = a.done;
         }
-        core.run(a.t0, a.K);
+        ChainNoHook<N> none;
+        core.run(a.t0, a.K, none);
         core.store(a);
     }
     if (STATS) {
         const uint32_t len_sum = env < a.n ? core.finished_length_sum(a.K) : 0u;
         store_block_stats(a.stats, blk, core.n_eps, len_sum, core.n_term, core.n_trunc);
     }
+}
+
+// k_chain_split<N>: the fused chain loop with a trajectory, warp-specialised as
+// k_cartpole_split: in a 512-thread workgroup the first four waves step the
+// block's 256 environments and write each step's row (2N + 2 obs words and
+// action | done << 8) to LDS; the last four waves store the rows.  Rows are
+// handed over in chunks of kChainHandSteps steps through two LDS buffers, one
+// workgroup barrier per chunk: between barriers c and c+1 the stepping waves
+// fill buffer (c+1) & 1 while the storing waves drain buffer c & 1.  Two-step
+// chunks keep the LDS at 2 x 2 x (8 N + 10) x 256 B (N = 4: 42 KB).
+constexpr uint32_t kChainHandSteps = 2;
+
+template <int N>
+struct ChainHandOver {
+    static constexpr int S = 2 * (N + 1);
+    float (*obs)[kChainHandSteps][S][kBlock];       // [2 buffers][step][word][env]
+    uint16_t (*act_done)[kChainHandSteps][kBlock];  // action | done byte << 8
+    uint32_t col;                                   // this thread's environment column
+    uint32_t i = 0u, buf = 0u;                      // step within the chunk, buffer
+    __device__ __forceinline__ void record(const ChainState<N>& st, uint32_t act, uint32_t d)
+    {
+#pragma unroll
+        for (int j = 0; j <= N; ++j) {
+            obs[buf][i][2 * j][col] = st.q[j];
+            obs[buf][i][2 * j + 1][col] = st.qd[j];
+        }
+        act_done[buf][i][col] = (uint16_t)(act | (d << 8));
+    }
+    __device__ __forceinline__ void advance()
+    {
+        if (++i == kChainHandSteps) {
+            i = 0u;
+            buf ^= 1u;
+            __syncthreads();
+        }
+    }
+    // the barrier that hands over a last, partial chunk
+    __device__ __forceinline__ void flush()
+    {
+        if (i != 0u) __syncthreads();
+    }
+};
+
+// The storing waves' copy of one recorded step (row `row` of the call):
+// byte planes first, then the obs words and the reward.
+template <int N>
+__device__ __forceinline__ void store_chain_row(const ChainArgs& a, size_t row, uint32_t off4, uint32_t off1,
+                                                const float (*obs)[kBlock], const uint16_t* act_done, uint32_t col)
+{
+    constexpr int S = 2 * (N + 1);
+    const size_t plane = a.n;
+    float v[S];
+#pragma unroll
+    for (int j = 0; j < S; ++j) v[j] = obs[j][col];
+    const uint32_t ad = act_done[col];
+    float* o = a.obs + row * S * plane;
+    *at(a.action + row * plane, off1) = (uint8_t)ad;
+    *at(a.done + row * plane, off1) = (uint8_t)(ad >> 8);
+#pragma unroll
+    for (int j = 0; j < S; ++j) *at(o + j * plane, off4) = v[j];
+    *at(a.reward + row * plane, off4) = 1.0f;
+}
+
+template <int N, bool STATS>
+__global__ __launch_bounds__(2 * kBlock) void k_chain_split(ChainArgs a)
+{
+    constexpr int S = 2 * (N + 1);
+    __shared__ float lds_obs[2][kChainHandSteps][S][kBlock];
+    __shared__ uint16_t lds_ad[2][kChainHandSteps][kBlock];
+    const uint32_t blk = xcd_block();
+    const uint32_t col = threadIdx.x % kBlock;
+    const uint32_t env = blk * kBlock + col;
+    const bool live = env < a.n;
+    uint32_t c0 = 0u, c1 = 0u, c2 = 0u, c3 = 0u;
+    if (threadIdx.x < kBlock) {
+        // stepping waves; threads past n step the chain at rest so that every
+        // wave passes the same barriers, and record nothing the storing side keeps
+        ChainCore<N, false, STATS> core(a.c, env);
+        if (live) {
+            core.load(a);
+        } else {
+#pragma unroll
+            for (int j = 0; j <= N; ++j) {
+                core.s.q[j] = 0.0f;
+                core.s.qd[j] = 0.0f;
+            }
+            core.ep = 0u;
+        }
+        ChainHandOver<N> h{lds_obs, lds_ad, col};
+        core.run(a.t0, a.K, h);
+        h.flush();
+        if (live) {
+            core.store(a);
+            c0 = core.n_eps;
+            c1 = core.finished_length_sum(a.K);
+            c2 = core.n_term;
+            c3 = core.n_trunc;
+        }
+    } else {
+        // storing waves: chunk c is complete after the c-th barrier
+        const uint32_t off4 = env * 4u, off1 = env;
+        const uint32_t n_chunks = a.K / kChainHandSteps + (a.K % kChainHandSteps != 0u ? 1u : 0u);
+        for (uint32_t c = 0; c < n_chunks; ++c) {
+            __syncthreads();
+            const uint32_t b = c & 1u, k0 = c * kChainHandSteps, m = min(kChainHandSteps, a.K - k0);
+            if (live) {
+                for (uint32_t i = 0; i < m; ++i)
+                    store_chain_row<N>(a, (size_t)k0 + i, off4, off1, lds_obs[b][i], lds_ad[b][i], col);
+            }
+        }
+    }
+    if (STATS) store_block_stats<2 * kBlock>(a.stats, blk, c0, c1, c2, c3);
 }
 
 // Initial state of every environment (episode beginning at step 0).

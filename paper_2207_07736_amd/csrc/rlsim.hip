@@ -251,10 +251,24 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
     return hipGetLastError();
 }
 
+// Fewest steps per call for which a trajectory-recording chain call runs the
+// warp-specialised chain kernel.
+constexpr uint32_t kChainSplitMinSteps = 16u;
+
 template <bool REC, bool STATS>
 hipError_t launch_chain(const ChainArgs& a, uint32_t N, hipStream_t s)
 {
     const dim3 grid(grid_for(a.n)), block(kBlock);
+    if (REC && a.K >= kChainSplitMinSteps) {
+        const dim3 wide_block(2 * kBlock);
+        switch (N) {
+        case 1: hipLaunchKernelGGL((k_chain_split<1, STATS>), grid, wide_block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_chain_split<2, STATS>), grid, wide_block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((k_chain_split<3, STATS>), grid, wide_block, 0, s, a); break;
+        default: hipLaunchKernelGGL((k_chain_split<4, STATS>), grid, wide_block, 0, s, a); break;
+        }
+        return hipGetLastError();
+    }
     switch (N) {
     case 1: hipLaunchKernelGGL((k_chain_fused<1, REC, STATS>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_chain_fused<2, REC, STATS>), grid, block, 0, s, a); break;

@@ -53,6 +53,24 @@ def test_chain_ragged_sizes(N, n):
         assert r["done"].any()
 
 
+@pytest.mark.parametrize("N", [1, 2, 3, 4])
+@pytest.mark.parametrize("n", [1, 63, 65, 257, 1000])
+def test_chain_warp_specialised_shapes(N, n):
+    """Trajectory calls of K >= 16 steps run the warp-specialised chain kernel
+    (rows handed from stepping to storing waves in 2-step chunks): K on and
+    off the chunk size around the threshold, blocks whose stepping waves are
+    partly or wholly past n, with and without the block statistics."""
+    sched = [15, 16, 17, 18, 33, 2, 64]
+    T = sum(sched)
+    print(f"chain split N={N} n={n} sched={sched}", flush=True)
+    r = oracle_run(n, T, sched, seed=40 + N, links=N)
+    for stats in (True, False):
+        g = gpu_run(n, T, sched, seed=40 + N, stats=stats, links=N)
+        assert_bit_equal(g, r)
+        if stats:
+            _stats_equal(g["stats"], r["stats"])
+
+
 @pytest.mark.parametrize("N", [2, 4])
 @pytest.mark.parametrize("seed", workloads.PARITY_SEEDS)
 def test_chain_seeds(N, seed):

@@ -100,3 +100,27 @@ def test_one_launch_per_policy_step_call(hip):
     finally:
         sim.close()
     del dev
+
+
+@pytest.mark.parametrize("N", [1, 4])
+def test_one_launch_per_chain_step_call(hip, N):
+    """The chain model: one launch per call for K below and above the
+    warp-specialised kernel's threshold, with and without a trajectory."""
+    from paper_2207_07736_amd import Simulator, Trajectory
+    s = torch.cuda.Stream()
+    n = 3000
+    sim = Simulator(n, 0, workloads.CARTPOLE, stream=s, links=N)
+    try:
+        sim.reset(1)
+        tr = Trajectory(300, n, S=sim.S)
+        torch.cuda.synchronize()
+        for K in (1, 15, 16, 300):
+            types = _captured_node_types(hip, s, lambda: sim.step(K, tr.rows(0, K)))
+            assert types == [HIP_NODE_KERNEL], (N, K, types)
+        types = _captured_node_types(hip, s, lambda: sim.step(300, None))
+        assert types == [HIP_NODE_KERNEL]
+        types = _captured_node_types(hip, s, lambda: sim.reset(2))
+        assert types == [HIP_NODE_KERNEL]
+        del tr
+    finally:
+        sim.close()
