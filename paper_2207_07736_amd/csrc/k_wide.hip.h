@@ -146,7 +146,14 @@ __device__ __forceinline__ void replay_uniform(float (&s)[W], const float (&pa)[
 #define RM_LEAF2(R, b0, b1) RM_CAT(RM_ENV_, b0)(R, 0) RM_CAT(RM_ENV_, b1)(R, 1)
 #define RM_LEAF4(R, b0, b1, b2, b3) RM_LEAF2(R, b0, b1) RM_CAT(RM_ENV_, b2)(R, 2) RM_CAT(RM_ENV_, b3)(R, 3)
 #define RM_TEST(u, lab) "s_bitcmp1_b32 %[" #u "], %[c]\n s_cbranch_scc1 " #lab "%=\n"
-#define RM_TO_TAIL "s_branch Lm_tail%=\n"
+// every leaf but the last carries its own copy of the loop tail (done test,
+// counter, loop branch), so a step takes one taken branch fewer than with a
+// jump to a shared tail (262,144 envs x 500 steps: D = 256 1.73 against
+// 1.84 ms, D = 512 2.43-2.47 against 2.46-2.56 ms)
+#define RM_TO_TAIL                                                \
+    "s_bitcmp1_b32 %[dor], %[c]\n s_cbranch_scc1 Lm_zero%=\n"     \
+    "s_add_u32 %[c], %[c], 1\n s_cmp_lt_u32 %[c], %[m]\n"          \
+    "s_cbranch_scc1 Lm_step%=\n s_branch Lm_end%=\n"
 #define RM_CLEAR(R, e, d, next)                                  \
     "s_bitcmp1_b32 %[" #d "], %[c]\n s_cbranch_scc0 " #next "%=\n" R(RM_ZERO, e) #next "%=:\n"
 #define RM_OUT_S(e, i) [s##e##_##i] "+v"(s##e[i]),
