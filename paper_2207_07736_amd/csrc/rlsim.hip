@@ -25,6 +25,7 @@ struct rlsim {
     uint32_t links = 0;         // chain links N (chain model)
     uint32_t S = 4;             // simulator state words: 4, or 2N + 2 for the chain
     int device = 0;
+    uint32_t cus = 1;           // compute units of the device (persistent-grid size)
     hipStream_t stream = nullptr;
     rlsim_cfg cfg{};
     DevParams dp{};
@@ -221,7 +222,7 @@ constexpr uint32_t kSplitPadMinSteps = 64u;
 constexpr uint32_t kMaxStateWords = (1u << 24) + 4u;
 
 template <bool REC, bool STATS>
-hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
+hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s)
 {
     const dim3 grid(grid_for(a.n)), block(kBlock);
     if (!wide) {
@@ -238,15 +239,18 @@ hipError_t launch_step(const StepArgs& a, bool wide, hipStream_t s)
     } else {
         // one environment per wave in the replay (wave-uniform bits), W words
         // per lane; E environments replayed together where that pays
-        // (262,144 envs x 500 steps: D = 256 1.84 / 1.98 / 2.24 ms for E = 4 / 2
-        // / 1, D = 512 3.10 / 2.55 / 2.81 ms, D = 1,024 E = 2 5.0 against E = 1
-        // 3.94 ms: four environments of 8 words, or two of 16, take the
-        // kernel past 128 VGPRs and below four waves per SIMD)
-        if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, REC, STATS, 4>), grid, block, 0, s, a);
-        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, REC, STATS, 2>), grid, block, 0, s, a);
-        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, REC, STATS>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_cartpole_wide<64, REC, STATS>), grid, block, 0, s, a);
+        // (262,144 envs x 500 steps, phases not overlapped: D = 256 1.84 / 1.98 /
+        // 2.24 ms for E = 4 / 2 / 1, D = 512 3.10 / 2.55 / 2.81 ms, D = 1,024
+        // E = 2 5.0 against E = 1 3.94 ms: four environments of 8 words, or two
+        // of 16, take the kernel past 128 VGPRs and below four waves per SIMD).
+        // One persistent workgroup per CU, of as many waves as the replay's
+        // registers allow four of per SIMD (three for W = 32, two for W = 64).
+        const dim3 pgrid(min(grid_for(a.n), cus));
+        if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, 1, 12, REC, STATS>), pgrid, dim3(768), 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_wide<64, 1, 8, REC, STATS>), pgrid, dim3(512), 0, s, a);
     }
     return hipGetLastError();
 }
@@ -374,6 +378,14 @@ int rlsim_create(uint32_t n_envs, uint32_t state_words, const rlsim_cfg* cfg, rl
         delete h;
         return rc;
     }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+    if (e != hipSuccess) {
+        int rc = hip_fail(nullptr, e, "rlsim_create: hipDeviceGetAttribute");
+        delete h;
+        return rc;
+    }
+    h->cus = cus > 0 ? (uint32_t)cus : 1u;
     const size_t n = n_envs;
     e = hipMalloc(&h->cart, (size_t)S * n * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&h->ep, n * sizeof(uint32_t));
@@ -516,10 +528,10 @@ int rlsim_step_fused(rlsim_t* h, uint32_t K, const rlsim_policy* policy, const r
         h->t += K;
         return RLSIM_OK;
     }
-    if (rec && stats) e = launch_step<true, true>(a, h->wide, h->stream);
-    else if (rec) e = launch_step<true, false>(a, h->wide, h->stream);
-    else if (stats) e = launch_step<false, true>(a, h->wide, h->stream);
-    else e = launch_step<false, false>(a, h->wide, h->stream);
+    if (rec && stats) e = launch_step<true, true>(a, h->wide, h->cus, h->stream);
+    else if (rec) e = launch_step<true, false>(a, h->wide, h->cus, h->stream);
+    else if (stats) e = launch_step<false, true>(a, h->wide, h->cus, h->stream);
+    else e = launch_step<false, false>(a, h->wide, h->cus, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "rlsim_step_fused: launch");
     h->t += K;
     return RLSIM_OK;
