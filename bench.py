@@ -28,10 +28,12 @@ import workloads  # noqa: E402
 METRIC = "env-steps/sec at 1 MI355X; achieved HBM GB/s vs peak; fused/unfused speedup"
 HBM_PEAK_GBS = 8000.0
 # fp32 VALU peak in lane operations (one FMA or multiply per lane) per second:
-# the published 157.3 TFLOP/s fp32 vector rate counts an FMA as two flops.
-# Plain (non-packed) v_fma_f32 / v_mul_f32 reach it on this part: a
-# store-free chain benchmark measured 5.6e13 / 6.5e13 lane-ops/s at 8 waves
-# per SIMD, above the 3.9e13 a four-cycle wave64 issue would allow.
+# the published 157.3 TFLOP/s fp32 vector rate, an FMA counted as two flops.
+# That figure counts two FMAs per lane per cycle, which only packed fp32
+# instructions reach; the kernels use none.  Plain v_fma_f32 issues at half of
+# it (3.83e13 lane-ops/s measured by rlsim_probe_issue at eight waves per SIMD,
+# a four-cycle wave64 issue), v_mul_f32 at 6.3e13, so a padding replay with
+# random actions (half FMAs, half multiplies) is capped near 0.61 of this peak.
 VALU_LANE_OPS_PER_S = 157.3e12 / 2
 COPY_BYTES = 1 << 30        # size of the plain copy used to calibrate the HBM byte counters
 
@@ -143,16 +145,24 @@ hbm_bytes_per_launch: {hbm:.0f}
     return path
 
 
-def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int, D: int = 0, policy=None) -> float:
+def _oracle_slices(n_slice_envs: int, starts, T: int, seed: int, threads: int, D: int = 0, policy=None,
+                   links: int = 0) -> float:
     """Wall seconds for the oracle to run T recorded steps of each env slice
-    [start, start + n_slice_envs), `threads` slices at a time.  Each slice is
-    its own oracle instance; the oracle's C loop runs outside the GIL."""
+    [start, start + n_slice_envs), `threads` slices at a time (links > 0: the
+    chain model).  Each slice is its own oracle instance; the oracle's C loop
+    runs outside the GIL."""
     import concurrent.futures as cf
 
     import oracle
     params = oracle.make_params(**workloads.CARTPOLE)
 
     def one(start):
+        if links:
+            sim = oracle.ChainSim(n_slice_envs, links, params, env0=start)
+            sim.reset(seed)
+            t0 = time.perf_counter()
+            sim.step(T)
+            return time.perf_counter() - t0
         sim = oracle.Sim(n_slice_envs, D, params, env0=start)
         sim.reset(seed)
         t0 = time.perf_counter()
@@ -245,6 +255,15 @@ def cpu_other_workloads(threads: int) -> dict:
         sec = _oracle_slices(n_slice, starts, T, w["seed"], threads, policy=pol)
         rows[dtype] = {"value": n_slice * threads * T / sec, "unit": "env-steps/s",
                        "sample": f"{threads} slices x {n_slice} envs x {T} steps (policy, value head), {sec:.1f} s wall"}
+    out[w["name"]] = rows
+    w = workloads.CHAIN_SWEEP
+    rows = {}
+    for N in w["N"]:
+        n_slice = 32768 // threads
+        starts = [i * (w["n"] // threads) for i in range(threads)]
+        sec = _oracle_slices(n_slice, starts, w["T"], w["seed"], threads, links=N)
+        rows[f"N{N}"] = {"value": n_slice * threads * w["T"] / sec, "unit": "env-steps/s",
+                         "sample": f"{threads} slices x {n_slice} envs x {w['T']} steps, {sec:.1f} s wall"}
     out[w["name"]] = rows
     return out
 
