@@ -259,7 +259,7 @@ def cpu_other_workloads(threads: int) -> dict:
     w = workloads.CHAIN_SWEEP
     rows = {}
     for N in w["N"]:
-        n_slice = 32768 // threads
+        n_slice = 262144 // threads                              # about 0.3-1 s of oracle work per N
         starts = [i * (w["n"] // threads) for i in range(threads)]
         sec = _oracle_slices(n_slice, starts, w["T"], w["seed"], threads, links=N)
         rows[f"N{N}"] = {"value": n_slice * threads * w["T"] / sec, "unit": "env-steps/s",
