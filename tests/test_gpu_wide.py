@@ -1,8 +1,10 @@
 """GPU parity of the wide-padding kernels (the paper's state-size factor S).
 
-Beyond 16 padding words per environment the library switches to the two-phase
-kernel (cart-pole pass leaves action/done bits in LDS, then lane groups replay
-the padding recurrence with the words in registers).  Everything is compared
+Beyond 64 padding words per environment the library switches to the two-phase
+kernel (the cart-pole pass leaves action/done bits in LDS, then waves replay
+the padding recurrence with the words in registers, pipelined across the
+256-env blocks of a persistent workgroup); up to 64 words stay in each
+thread's registers.  Everything is compared
 bit for bit with the oracle: trajectory, block statistics, cart-pole state,
 all padding words and episode counters.
 """
@@ -23,9 +25,10 @@ def _need_gpu():
     import paper_2207_07736_amd  # noqa: F401
 
 
-# D values cover every kernel shape: 8x8 lane groups (<= 64 words), one env per
-# wave with 4/8/16/32/64 words per lane, ragged rows (D not a multiple of 4 or
-# of the chunk) and several word chunks per env (D > 4096).
+# D values cover every kernel shape: register-resident words (<= 64), one env
+# per wave with 4/8/16/32/64 words per lane (four or two envs per scalar
+# decision up to 512 words), ragged rows (D not a multiple of 4 or of the
+# chunk) and several word chunks per env (D > 4096).
 @pytest.mark.parametrize("D", [17, 32, 33, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
 def test_wide_padding_bit_exact(D):
     n = 260                                   # two stats blocks, ragged tail
@@ -46,6 +49,32 @@ def test_wide_long_launch_crosses_chunks(D):
     g = gpu_run(n, T, [T], D=D, seed=workloads.PARITY_SEEDS[2])
     r = oracle_run(n, T, [T], D=D, seed=workloads.PARITY_SEEDS[2])
     assert_bit_equal(g, r)
+
+
+@pytest.mark.parametrize("D", [72, 300, 1100])
+def test_wide_pipeline_several_blocks_per_workgroup(D):
+    """More 256-env blocks than the persistent grid has workgroups (one per CU):
+    workgroup 0 runs blocks 0 and 256 one after the other, the last block is
+    partial, and K = 800 takes two 512-step rounds per block, so several items
+    of one block pass through the pipeline; a second call of K = 300 follows.
+    The columns of blocks 0, 256 and the partial last one -- the trajectory,
+    the cart-pole state and every padding word -- and their statistics rows
+    equal the oracle's slices at the same global ids (D = 72, 300 and 1,100 take
+    the 4-, 8- and 32-words-per-lane shapes, of 16, 16 and 12 waves)."""
+    n = 256 * 257 + 100
+    T, sched = 1100, [800, 300]
+    slices = [(0, 256), (256 * 256, 256 * 257), (256 * 257, n)]
+    print(f"wide pipeline D={D} n={n} sched={sched}", flush=True)
+    g = gpu_run(n, T, sched, D=D, seed=21, slices=slices)
+    refs = [oracle_run(b - a, T, sched, D=D, seed=21, env0=a) for a, b in slices]
+    want = {k: np.concatenate([r[k] for r in refs], axis=-1) for k in ("obs", "action", "reward", "done", "state")}
+    want["ep"] = np.concatenate([r["ep"] for r in refs])
+    want["t"] = refs[0]["t"]
+    assert_bit_equal(g, want, keys=("obs", "action", "reward", "done", "state", "ep"))
+    for call, gs in enumerate(g["stats"]):
+        for (a, b), r in zip(slices, refs):
+            rows = r["stats"][call]
+            assert np.array_equal(gs[a // 256:a // 256 + len(rows)], rows), (call, a)
 
 
 def test_wide_edge_configs():
