@@ -655,15 +655,19 @@ def wide_only(D: int, steps: int, warmup: int, copy_calibration: bool = False) -
     return 0
 
 
+FILL_SHAPES = (1, 4, 64, 275, 1024)     # float4 stores per thread; 275: a trajectory workgroup's volume
+
+
 def store_ceiling_only(steps: int) -> int:
-    """The headline's store ceiling against a plain fill (for counters): the
+    """The headline's store ceiling against plain fills (for counters): the
     store-only probe writing the 4,194,304-env x 200-row trajectory (seven
     planes per row, byte planes first), then torch's fill of one contiguous
-    buffer of the same 18.45 GB, then the headline launch itself, each `steps`
-    times, with the per-launch times printed."""
+    buffer of the same 18.45 GB, then the fill probe over that buffer with
+    FILL_SHAPES float4 stores per thread, then the headline launch itself, each
+    `steps` times, with the per-launch times printed."""
     import torch
     from paper_2207_07736_amd import Simulator, Trajectory
-    from paper_2207_07736_amd.probe import probe_store
+    from paper_2207_07736_amd.probe import probe_fill, probe_store
     w = workloads.WORKLOADS[workloads.HEADLINE]
     n, T = w["n"], w["T"]
     stream = torch.cuda.current_stream()
@@ -684,6 +688,8 @@ def store_ceiling_only(steps: int) -> int:
     timed("store_probe_ms", lambda: probe_store(n, T, traj.obs, traj.action, traj.reward, traj.done, stream))
     flat = torch.empty(n * T * workloads.TRAJ_BYTES_PER_ENV_STEP // 4, dtype=torch.float32, device="cuda")
     timed("plain_fill_ms", lambda: flat.fill_(1.0))
+    for per in FILL_SHAPES:
+        timed(f"fill_probe_{per}_per_thread_ms", lambda per=per: probe_fill(flat, per, stream))
     del flat
     sim = Simulator(n, 0, workloads.CARTPOLE, stream=stream)
     sim.reset(w["seed"])

@@ -2,7 +2,8 @@
  * rlsim_probe.h -- C ABI of the measurement aids beside librlsim.so
  * (librlsim_probe.so): the store-only probe of the trajectory layout, a
  * read/write stream probe, the error probe of the policy kernel's
- * elementwise functions, and an instruction-rate probe.
+ * elementwise functions, an instruction-rate probe and a fill probe of store
+ * kernel shapes.
  *
  * The fused simulator kernel's unavoidable work is writing the trajectory
  * (section "Simulator Kernel Fusion": fusion removes the state round trips,
@@ -90,6 +91,20 @@ int rlsim_probe_stream(uint64_t n4, float* s, const float* a, const float* b, vo
  * Errors: -1 if kind > 6, blocks == 0 or > 2^20, iters == 0 or > 2^22 (kind
  * 5: > 2^19), or out is NULL or not 4-byte aligned; -3 if the launch fails. */
 int rlsim_probe_issue(uint32_t kind, uint32_t blocks, uint32_t iters, float* out, void* stream);
+
+/* Store-rate probe of kernel shape (section "Simulator Kernel Fusion": what a
+ * fused kernel's trajectory stores can reach depends on how they are issued):
+ * a plain fill of n4 float4 at dst (caller-owned DEVICE, 16-byte aligned) by
+ * workgroups of 256 threads, each thread storing per_thread float4 -- thread t
+ * of workgroup b the indices b 256 per_thread + t + 256 j, j < per_thread --
+ * so per_thread = 1 is one store per thread over a grid of many small
+ * workgroups and large per_thread a long store loop per thread over a
+ * workgroup-contiguous chunk (per_thread = 275 is the 1,126,400 bytes a
+ * trajectory workgroup of 256 environments writes in 200 steps).
+ * dst[i] = (v, v + 1, v + 2, v + 3) with v = i mod 2^20 (exact in fp32).
+ * Errors: -1 if n4 == 0, per_thread == 0 or > 2^20, the grid would reach 2^31
+ * workgroups, or dst is NULL or not 16-byte aligned; -3 if the launch fails. */
+int rlsim_probe_fill(uint64_t n4, uint32_t per_thread, float* dst, void* stream);
 
 #ifdef __cplusplus
 }

@@ -61,6 +61,7 @@ extern "C" int rlsim_probe_store(uint32_t n, uint32_t K, float* obs, uint8_t* ac
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
+#include "fill_probe.hip.h"
 #include "issue_probe.hip.h"
 #include "math_probe.hip.h"
 #include "stream_probe.hip.h"

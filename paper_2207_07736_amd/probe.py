@@ -1,7 +1,8 @@
 """Thin ctypes binding of librlsim_probe.so (include/rlsim_probe.h): the
 store-only probe of the trajectory layout, a read/write stream probe, the
-error probe of the policy kernel's elementwise functions and the
-instruction-rate probe, measurement aids.  Argument
+error probe of the policy kernel's elementwise functions, the
+instruction-rate probe and the fill probe of store kernel shapes, measurement
+aids.  Argument
 marshalling only; fails loudly if the library has not been built."""
 from __future__ import annotations
 
@@ -10,7 +11,8 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
-PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream", "rlsim_probe_issue")
+PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream", "rlsim_probe_issue",
+                 "rlsim_probe_fill")
 ISSUE_KINDS = ("fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul")
 
 
@@ -27,6 +29,8 @@ def _load():
     L.rlsim_probe_stream.restype = ctypes.c_int
     L.rlsim_probe_issue.argtypes = [u32, u32, u32, vp, vp]
     L.rlsim_probe_issue.restype = ctypes.c_int
+    L.rlsim_probe_fill.argtypes = [ctypes.c_uint64, u32, vp, vp]
+    L.rlsim_probe_fill.restype = ctypes.c_int
     return L
 
 
@@ -78,3 +82,15 @@ def probe_issue(kind: str, blocks: int, iters: int, out, stream=None) -> None:
     rc = probe_lib.rlsim_probe_issue(ISSUE_KINDS.index(kind), int(blocks), int(iters), _ptr(out), st)
     if rc != 0:
         raise ValueError(f"rlsim_probe_issue rejected its arguments (status {rc})")
+
+
+def probe_fill(dst, per_thread: int, stream=None) -> None:
+    """Fill the float32 device tensor dst (a multiple of 4 elements, 16-byte
+    aligned) with per_thread float4 stores per thread; raises ValueError on a
+    rejected argument."""
+    if dst.numel() % 4:
+        raise ValueError("probe_fill needs a multiple of 4 floats")
+    st = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    rc = probe_lib.rlsim_probe_fill(dst.numel() // 4, int(per_thread), _ptr(dst), st)
+    if rc != 0:
+        raise ValueError(f"rlsim_probe_fill rejected its arguments (status {rc})")

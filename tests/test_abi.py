@@ -214,6 +214,12 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.rlsim_probe_issue(5, 1, (1 << 19) + 1, 16, None) == -1
     assert L.rlsim_probe_issue(0, 1, 1, None, None) == -1
     assert L.rlsim_probe_issue(0, 1, 1, 18, None) == -1               # misaligned out
+    assert L.rlsim_probe_fill(0, 1, 16, None) == -1
+    assert L.rlsim_probe_fill(16, 0, 16, None) == -1
+    assert L.rlsim_probe_fill(16, (1 << 20) + 1, 16, None) == -1
+    assert L.rlsim_probe_fill(1 << 40, 1, 16, None) == -1              # grid of 2^32 workgroups
+    assert L.rlsim_probe_fill(16, 1, None, None) == -1
+    assert L.rlsim_probe_fill(16, 1, 20, None) == -1                  # misaligned dst
 
 
 def test_probe_issues_each_steps_stores_back_to_back(tmp_path):

@@ -76,6 +76,24 @@ def test_stream_probe_values():
     assert np.array_equal(ta.cpu().numpy(), a) and np.array_equal(tb.cpu().numpy(), b)
 
 
+@pytest.mark.parametrize("per", [1, 4, 275])
+def test_fill_probe_values(per):
+    """rlsim_probe_fill writes float4 i as (v, v + 1, v + 2, v + 3), v = i mod
+    2^20, at every index of a buffer whose size is no multiple of a
+    workgroup's chunk, and nothing past it."""
+    import numpy as np
+    from paper_2207_07736_amd.probe import probe_fill
+    n4 = 3 * 256 * 275 + 1234
+    buf = torch.full((4 * n4 + 64,), -7.0, dtype=torch.float32, device="cuda")
+    probe_fill(buf[:4 * n4], per)
+    torch.cuda.synchronize()
+    got = buf.cpu().numpy()
+    v = (np.arange(n4, dtype=np.int64) & 0xFFFFF).astype(np.float32)
+    want = np.stack([v, v + 1, v + 2, v + 3], axis=1).reshape(-1)
+    assert np.array_equal(got[:4 * n4], want)
+    assert np.all(got[4 * n4:] == -7.0)
+
+
 @pytest.mark.parametrize("kind", ["fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul"])
 def test_issue_probe_values(kind):
     """rlsim_probe_issue runs the instruction chains it claims: every thread's
