@@ -77,6 +77,45 @@ def test_wide_pipeline_several_blocks_per_workgroup(D):
             assert np.array_equal(gs[a // 256:a // 256 + len(rows)], rows), (call, a)
 
 
+@pytest.mark.parametrize("D", [72, 300])
+def test_wide_pipeline_without_trajectory(D):
+    """The wide kernel's forms without a trajectory, at the multi-block size of
+    the test above: a call with traj = NULL and a statistics-only call leave the
+    same state as the recording call, the statistics equal the recording call's,
+    and both match the oracle's slices of the first and last blocks."""
+    from paper_2207_07736_amd import Simulator, Trajectory, stats_only
+    n, T, seed = 256 * 257 + 100, 700, 23
+    states, stats = [], []
+    for form in ("traj", "none", "stats"):
+        sim = Simulator(n, D, workloads.CARTPOLE)
+        try:
+            sim.reset(seed)
+            if form == "traj":
+                tr = Trajectory(T, n)
+                sim.step(T, tr.rows(0, T))
+                stats.append(tr.block_stats.clone())
+                del tr
+            elif form == "none":
+                sim.step(T, None)
+            else:
+                st = torch.zeros(((n + 255) // 256, 4), dtype=torch.int32, device="cuda")
+                sim.step(T, stats_only(st, n))
+                stats.append(st)
+            torch.cuda.synchronize()
+            states.append(sim.get_state())
+        finally:
+            sim.close()
+    for st, ep, t in states[1:]:
+        assert np.array_equal(st.view(np.uint32), states[0][0].view(np.uint32))
+        assert np.array_equal(ep, states[0][1]) and t == T
+    assert torch.equal(stats[0], stats[1])
+    for a, b in ((0, 256), (256 * 257, n)):
+        r = oracle_run(b - a, T, [T], D=D, seed=seed, env0=a)
+        assert np.array_equal(states[0][0][:, a:b].view(np.uint32), r["state"].view(np.uint32))
+        assert np.array_equal(stats[1].cpu().numpy().view(np.uint32)[a // 256:a // 256 + len(r["stats"][0])],
+                              r["stats"][0])
+
+
 def test_wide_edge_configs():
     cfg = workloads.cartpole(max_episode_steps=7, no_termination=1)
     g = gpu_run(200, 60, [13, 47], D=70, seed=1, cfg=cfg)
