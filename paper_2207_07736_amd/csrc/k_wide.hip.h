@@ -436,7 +436,7 @@ __global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
         __syncthreads();
     } else {
         for (uint32_t j = 0; j <= n_items; ++j) {
-            // the statistics of a block whose last item ended in iteration j - 1
+            // the statistics of a block whose last item was stepped in iteration j - 1
             if (STATS && j >= 1u && (j - 1u) % rounds == rounds - 1u && threadIdx.x < 4u * 64u + 4u &&
                 threadIdx.x >= 4u * 64u) {
                 const uint32_t m = (j - 1u) / rounds, q = threadIdx.x - 4u * 64u;
