@@ -75,5 +75,18 @@ def asm(out_path: str, src: str = SRC) -> str:
     return out_path
 
 
+def device_object(out_path: str, src: str = SRC) -> str:
+    """Write the gfx950 code object of a source's device code (for inspection
+    with llvm-objdump)."""
+    bundled = out_path + ".bundle"
+    cmd = [HIPCC, *[f for f in FLAGS if f not in ("-shared", "-fPIC")], "-I", INCLUDE,
+           "--cuda-device-only", "-c", "-o", bundled, src]
+    subprocess.run(cmd, check=True)
+    bundler = os.path.join(os.path.dirname(os.path.realpath(HIPCC)), "..", "llvm", "bin", "clang-offload-bundler")
+    subprocess.run([bundler, "--unbundle", "--type=o", f"--input={bundled}",
+                    "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", f"--output={out_path}"], check=True)
+    return out_path
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

@@ -1,6 +1,6 @@
-// k_wide.hip.h -- cart-pole with a wide padding state (D > 64 words per
+// k_wide.hip.h -- cart-pole with a wide padding state (D > 32 words per
 // environment, the state-size factor S of the paper's "Simulator Complexity"),
-// too many to keep in one thread's registers.  Each 512-step round of a block
+// more than one thread's registers hold cheaply.  Each 512-step round of a block
 // of 256 environments runs the cart-pole loop one thread per environment and
 // records the action and done bits in LDS (phase 1); the padding recurrence is
 // then replayed from those bits with each environment's words spread over the
@@ -339,6 +339,159 @@ __device__ __forceinline__ void replay_env(const StepArgs& a, const uint32_t* ld
     }
 }
 
+// ---------------------------------------------------------------------------
+// One padding word per lane (at most 64 words), eight environments per step.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kJtGroup = 8;                     // environments per replay group
+
+// Phase-1 hook for the jump-table replay: each step's action and done bits of
+// the wave's 64 environments (one ballot each), kept as one byte per group of
+// eight consecutive environments -- bit e of byte g is environment 8 g + e of
+// the wave -- in LDS rows [group][step].  Lane g of a wave writes its group's
+// bytes; a group with a live environment has a live writer (environments past n
+// are the wave's last lanes).
+struct ByteRecorder {
+    uint8_t* lds_u;      // [kBlock / kJtGroup][kChunk]
+    uint8_t* lds_d;
+    uint32_t lane, wave;
+    uint32_t k = 0u;     // step index within the round
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
+    __device__ __forceinline__ void operator()(uint32_t act, bool reset)
+    {
+        const uint64_t ub = __builtin_amdgcn_ballot_w64(act != 0u);
+        const uint64_t db = __builtin_amdgcn_ballot_w64(reset);
+        if (lane < 64u / kJtGroup) {
+            const uint32_t row = (wave * (64u / kJtGroup) + lane) * kChunk + k;
+            lds_u[row] = (uint8_t)(ub >> (kJtGroup * lane));
+            lds_d[row] = (uint8_t)(db >> (kJtGroup * lane));
+        }
+        ++k;
+    }
+    __device__ __forceinline__ void flush() {}
+};
+
+// The replay of up to 32 steps of one group in one asm block.  Step c reads
+// its action byte (byte c % 4 of u[c / 4]) and jumps with s_swappc_b64 to leaf
+// number byte of a table of 256 leaves, each eight in-place updates -- the
+// word of environment e takes v_fma_f32 (one rounding) when bit e is set and
+// v_mul_f32 otherwise -- that returns with s_setpc_b64; every leaf is 68 bytes
+// (eight 8-byte VOP3 instructions and the return), so leaf i starts at table +
+// 68 i.  A nonzero done byte calls the clearing routine, which zeroes the words
+// of the environments whose bit is set.  The 32 steps are unrolled; a second
+// copy tests the step count m before each step, for a last, partial word.
+// s80..s89 hold the table and routine addresses and the return addresses.
+#define JT_M(e) "v_mul_f32_e64 %[s" #e "], %[a" #e "], %[s" #e "]\n"
+#define JT_F(e) "v_fma_f32 %[s" #e "], %[a" #e "], %[s" #e "], %[b" #e "]\n"
+#define JT_OP0(e) JT_M(e)
+#define JT_OP1(e) JT_F(e)
+#define JT_LEAF(b0, b1, b2, b3, b4, b5, b6, b7)                                                            \
+    JT_OP##b0(0) JT_OP##b1(1) JT_OP##b2(2) JT_OP##b3(3) JT_OP##b4(4) JT_OP##b5(5) JT_OP##b6(6) JT_OP##b7(7) \
+        "s_setpc_b64 s[88:89]\n"
+#define JT_T0(b1, b2, b3, b4, b5, b6, b7) JT_LEAF(0, b1, b2, b3, b4, b5, b6, b7) JT_LEAF(1, b1, b2, b3, b4, b5, b6, b7)
+#define JT_T1(b2, b3, b4, b5, b6, b7) JT_T0(0, b2, b3, b4, b5, b6, b7) JT_T0(1, b2, b3, b4, b5, b6, b7)
+#define JT_T2(b3, b4, b5, b6, b7) JT_T1(0, b3, b4, b5, b6, b7) JT_T1(1, b3, b4, b5, b6, b7)
+#define JT_T3(b4, b5, b6, b7) JT_T2(0, b4, b5, b6, b7) JT_T2(1, b4, b5, b6, b7)
+#define JT_T4(b5, b6, b7) JT_T3(0, b5, b6, b7) JT_T3(1, b5, b6, b7)
+#define JT_T5(b6, b7) JT_T4(0, b6, b7) JT_T4(1, b6, b7)
+#define JT_T6(b7) JT_T5(0, b7) JT_T5(1, b7)
+#define JT_TABLE JT_T6(0) JT_T6(1)
+// one step: leaf call, then the done byte (SCC = byte != 0) and the call of
+// the clearing routine through an out-of-line stub
+#define JT_STEP(P, c, w, bc)                                     \
+    "s_bfe_u32 s84, %[u" #w "], " #bc "\n"                      \
+    "s_mul_i32 s84, s84, 68\n"                                   \
+    "s_add_u32 s86, s80, s84\n"                                  \
+    "s_addc_u32 s87, s81, 0\n"                                   \
+    "s_swappc_b64 s[88:89], s[86:87]\n"                          \
+    "s_bfe_u32 s85, %[d" #w "], " #bc "\n"                      \
+    "s_cbranch_scc1 Lj" #P "c" #c "_%=\n"                        \
+    "Lj" #P "r" #c "_%=:\n"
+#define JT_PSTEP(c, w, bc) "s_cmp_le_u32 %[m], " #c "\n s_cbranch_scc1 Ljend%=\n" JT_STEP(p, c, w, bc)
+#define JT_STUB(P, c) "Lj" #P "c" #c "_%=:\n s_swappc_b64 s[88:89], s[82:83]\n s_branch Lj" #P "r" #c "_%=\n"
+#define JT_WORD(X, P, w, c0, c1, c2, c3) \
+    X(P, c0, w, 0x80000) X(P, c1, w, 0x80008) X(P, c2, w, 0x80010) X(P, c3, w, 0x80018)
+#define JT_FSTEP(P, c, w, bc) JT_STEP(P, c, w, bc)
+#define JT_PSTEPX(P, c, w, bc) JT_PSTEP(c, w, bc)
+#define JT_STEPS(X, P)                                                                                   \
+    JT_WORD(X, P, 0, 0, 1, 2, 3) JT_WORD(X, P, 1, 4, 5, 6, 7) JT_WORD(X, P, 2, 8, 9, 10, 11)               \
+        JT_WORD(X, P, 3, 12, 13, 14, 15) JT_WORD(X, P, 4, 16, 17, 18, 19) JT_WORD(X, P, 5, 20, 21, 22, 23) \
+            JT_WORD(X, P, 6, 24, 25, 26, 27) JT_WORD(X, P, 7, 28, 29, 30, 31)
+#define JT_STUBS(P)                                                                                       \
+    JT_STUB(P, 0) JT_STUB(P, 1) JT_STUB(P, 2) JT_STUB(P, 3) JT_STUB(P, 4) JT_STUB(P, 5) JT_STUB(P, 6)      \
+        JT_STUB(P, 7) JT_STUB(P, 8) JT_STUB(P, 9) JT_STUB(P, 10) JT_STUB(P, 11) JT_STUB(P, 12)             \
+            JT_STUB(P, 13) JT_STUB(P, 14) JT_STUB(P, 15) JT_STUB(P, 16) JT_STUB(P, 17) JT_STUB(P, 18)      \
+                JT_STUB(P, 19) JT_STUB(P, 20) JT_STUB(P, 21) JT_STUB(P, 22) JT_STUB(P, 23) JT_STUB(P, 24)  \
+                    JT_STUB(P, 25) JT_STUB(P, 26) JT_STUB(P, 27) JT_STUB(P, 28) JT_STUB(P, 29)             \
+                        JT_STUB(P, 30) JT_STUB(P, 31)
+#define JT_CLR(e) "s_bitcmp1_b32 s85, " #e "\n s_cbranch_scc0 Ljz" #e "_%=\n v_mov_b32 %[s" #e "], 0\nLjz" #e "_%=:\n"
+#define JT_INA(e) [a##e] "v"(pa[e]),
+#define JT_INB(e) [b##e] "v"(pb[e]),
+#define JT_INU(e) [u##e] "s"(u[e]),
+#define JT_IND(e) [d##e] "s"(d[e]),
+#define JT_R8(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7)
+
+__device__ __forceinline__ void replay_jt(float (&s)[8], const float (&pa)[8], const float (&pb)[8],
+                                          const uint32_t (&u)[8], const uint32_t (&d)[8], uint32_t m)
+{
+    asm volatile("s_getpc_b64 s[80:81]\n"
+                 "Ljbase0_%=:\n"
+                 "s_add_u32 s80, s80, Ljtab%= - Ljbase0_%=\n"
+                 "s_addc_u32 s81, s81, 0\n"
+                 "s_getpc_b64 s[82:83]\n"
+                 "Ljbase1_%=:\n"
+                 "s_add_u32 s82, s82, Ljclr%= - Ljbase1_%=\n"
+                 "s_addc_u32 s83, s83, 0\n"
+                 "s_cmp_eq_u32 %[m], 32\n"
+                 "s_cbranch_scc0 Ljpart%=\n"
+                 JT_STEPS(JT_FSTEP, f)
+                 "s_branch Ljend%=\n"
+                 "Ljpart%=:\n"
+                 JT_STEPS(JT_PSTEPX, p)
+                 "s_branch Ljend%=\n"
+                 JT_STUBS(f) JT_STUBS(p)
+                 "Ljclr%=:\n" JT_R8(JT_CLR) "s_setpc_b64 s[88:89]\n"
+                 "Ljtab%=:\n" JT_TABLE
+                 "Ljend%=:\n"
+                 : [s0] "+v"(s[0]), [s1] "+v"(s[1]), [s2] "+v"(s[2]), [s3] "+v"(s[3]), [s4] "+v"(s[4]),
+                   [s5] "+v"(s[5]), [s6] "+v"(s[6]), [s7] "+v"(s[7])
+                 : JT_R8(JT_INA) JT_R8(JT_INB) JT_R8(JT_INU) JT_R8(JT_IND)[m] "s"(m)
+                 : "scc", "s80", "s81", "s82", "s83", "s84", "s85", "s86", "s87", "s88", "s89");
+}
+
+// Phase 2 of group g (columns 8 g .. 8 g + 7 of block blk): lane l holds word
+// l of each of the eight environments.
+__device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t* lds_u, const uint8_t* lds_d,
+                                                uint32_t steps, uint32_t blk, uint32_t g)
+{
+    const uint32_t lane = threadIdx.x % 64u;
+    float s[8], pa[8], pb[8];
+    size_t row[8];
+    bool on[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t env = blk * kBlock + g * kJtGroup + (uint32_t)e;
+        row[e] = (size_t)env * a.Dp + lane;
+        on[e] = env < a.n && lane < a.Dp;
+        s[e] = on[e] ? a.pad_s[row[e]] : 0.0f;
+        pa[e] = on[e] ? a.pad_a[row[e]] : 0.0f;
+        pb[e] = on[e] ? a.pad_b[row[e]] : 0.0f;
+    }
+    for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
+        const uint32_t* pu = reinterpret_cast<const uint32_t*>(lds_u + g * kChunk + w32 * 32u);
+        const uint32_t* pd = reinterpret_cast<const uint32_t*>(lds_d + g * kChunk + w32 * 32u);
+        uint32_t u[8], d[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            u[q] = __builtin_amdgcn_readfirstlane(pu[q]);
+            d[q] = __builtin_amdgcn_readfirstlane(pd[q]);
+        }
+        replay_jt(s, pa, pb, u, d, __builtin_amdgcn_readfirstlane(min(32u, steps - w32 * 32u)));
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        if (on[e]) a.pad_s[row[e]] = s[e];
+}
+
 // k_cartpole_wide<W, E, NW>: the two phases, overlapped across the blocks of a
 // persistent workgroup of NW waves (one workgroup per CU; workgroup g takes the
 // 256-env blocks g, g + G, ... of a grid of G).  A work item is one 512-step
@@ -357,6 +510,7 @@ template <int W, int E, int NW, bool REC, bool STATS>
 __global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
 {
     static_assert(NW >= 8 && NW <= 16, "the pipeline needs four stepping waves and at least four more");
+    static_assert(W != 1 || E == (int)kJtGroup, "one word per lane takes the eight-environment jump table");
     __shared__ uint32_t lds_u[2][kChunkWords * kBlock];
     __shared__ uint32_t lds_d[2][kChunkWords * kBlock];
     __shared__ uint32_t next_group[2];
@@ -387,7 +541,10 @@ __global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
             if (lane == 0u) g = atomicAdd(&next_group[sl], 1u);
             g = __builtin_amdgcn_readfirstlane(g);
             if (g >= n_groups) break;
-            if constexpr (E > 1) replay_group<W, E>(a, lds_u[sl], lds_d[sl], steps, blk, g * (uint32_t)E);
+            if constexpr (W == 1)
+                replay_group_jt(a, reinterpret_cast<const uint8_t*>(lds_u[sl]),
+                                reinterpret_cast<const uint8_t*>(lds_d[sl]), steps, blk, g);
+            else if constexpr (E > 1) replay_group<W, E>(a, lds_u[sl], lds_d[sl], steps, blk, g * (uint32_t)E);
             else replay_env<W>(a, lds_u[sl], lds_d[sl], steps, blk, g);
         }
     };
@@ -407,11 +564,17 @@ __global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
                 const uint32_t k0 = r * kChunk, steps = min(kChunk, a.K - k0);
                 // slot j & 1's counter was last used in iteration j - 1
                 if (threadIdx.x == 0u) next_group[j & 1u] = 0u;
-                BitRecorder rec{lds_u[j & 1u], lds_d[j & 1u], col};
                 if (live) {
                     if (REC) core.set_rows(a, k0);
-                    core.run(a.t0 + k0, steps, rec);
-                    rec.flush();
+                    if constexpr (W == 1) {
+                        ByteRecorder rec{reinterpret_cast<uint8_t*>(lds_u[j & 1u]),
+                                         reinterpret_cast<uint8_t*>(lds_d[j & 1u]), lane, wave};
+                        core.run(a.t0 + k0, steps, rec);
+                    } else {
+                        BitRecorder rec{lds_u[j & 1u], lds_d[j & 1u], col};
+                        core.run(a.t0 + k0, steps, rec);
+                        rec.flush();
+                    }
                 }
                 if (r + 1u == rounds) {
                     if (live) core.store(a);

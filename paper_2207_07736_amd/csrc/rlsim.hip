@@ -204,10 +204,11 @@ unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 
 // Largest padding count of the register-resident (one thread per env) kernel;
 // above it the two-phase wide kernel holds the words.  (262,144 envs x 500
-// steps: D = 64 1.23 ms with the 64 words in each thread's registers, 250
-// VGPRs, against 1.37 ms for the two-phase kernel replaying them on 8 lanes
-// per environment; D = 32 0.85 against 1.08 ms.)
-constexpr uint32_t kMaxRegisterWords = 64u;
+// steps: D = 32 0.82-0.87 ms in registers against 1.01-1.03 ms for the wide
+// kernel's eight-environment jump table, one word per lane, whose cost does not
+// shrink with D; D = 48 and 64 1.07-1.13 ms in registers, where every thread
+// updates all 64 words, against 0.99-1.03 ms.)
+constexpr uint32_t kMaxRegisterWords = 32u;
 // Fewest steps per call for which a trajectory-recording call runs the
 // warp-specialised kernel: without padding words, and with 1-4 padding words.
 // Below them the hand-over's pipeline fill and drain cost more than the faster
@@ -234,8 +235,7 @@ hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s
         else if (a.D <= 4u) hipLaunchKernelGGL((k_cartpole_fused<4, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 8u) hipLaunchKernelGGL((k_cartpole_fused<8, REC, STATS>), grid, block, 0, s, a);
         else if (a.D <= 16u) hipLaunchKernelGGL((k_cartpole_fused<16, REC, STATS>), grid, block, 0, s, a);
-        else if (a.D <= 32u) hipLaunchKernelGGL((k_cartpole_fused<32, REC, STATS>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_cartpole_fused<64, REC, STATS>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_fused<32, REC, STATS>), grid, block, 0, s, a);
     } else {
         // one environment per wave in the replay (wave-uniform bits), W words
         // per lane; E environments replayed together where that pays
@@ -243,10 +243,13 @@ hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s
         // 2.24 ms for E = 4 / 2 / 1, D = 512 3.10 / 2.55 / 2.81 ms, D = 1,024
         // E = 2 5.0 against E = 1 3.94 ms: four environments of 8 words, or two
         // of 16, take the kernel past 128 VGPRs and below four waves per SIMD).
-        // One persistent workgroup per CU, of as many waves as the replay's
-        // registers allow four of per SIMD (three for W = 32, two for W = 64).
+        // Up to 64 words: one word per lane, eight environments per step
+        // through the replay's jump table.  One persistent workgroup per CU, of
+        // as many waves as the replay's registers allow four of per SIMD (three
+        // for W = 32, two for W = 64).
         const dim3 pgrid(min(grid_for(a.n), cus));
-        if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, 1, 12, REC, STATS>), pgrid, dim3(768), 0, s, a);

@@ -1,9 +1,10 @@
 """GPU parity of the wide-padding kernels (the paper's state-size factor S).
 
-Beyond 64 padding words per environment the library switches to the two-phase
+Beyond 32 padding words per environment the library switches to the two-phase
 kernel (the cart-pole pass leaves action/done bits in LDS, then waves replay
 the padding recurrence with the words in registers, pipelined across the
-256-env blocks of a persistent workgroup); up to 64 words stay in each
+256-env blocks of a persistent workgroup; up to 64 words, one word per lane and
+eight environments per step through a jump table); up to 32 words stay in each
 thread's registers.  Everything is compared
 bit for bit with the oracle: trajectory, block statistics, cart-pole state,
 all padding words and episode counters.
@@ -25,10 +26,11 @@ def _need_gpu():
     import paper_2207_07736_amd  # noqa: F401
 
 
-# D values cover every kernel shape: register-resident words (<= 64), one env
-# per wave with 4/8/16/32/64 words per lane (four or two envs per scalar
-# decision up to 512 words), ragged rows (D not a multiple of 4 or of the
-# chunk) and several word chunks per env (D > 4096).
+# D values cover every kernel shape: register-resident words (<= 32), one word
+# per lane for eight envs at a time (33-64), one env per wave with
+# 4/8/16/32/64 words per lane (four or two envs per scalar decision up to 512
+# words), ragged rows (D not a multiple of 4 or of the chunk) and several word
+# chunks per env (D > 4096).
 @pytest.mark.parametrize("D", [17, 32, 33, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
 def test_wide_padding_bit_exact(D):
     n = 260                                   # two stats blocks, ragged tail
@@ -51,7 +53,7 @@ def test_wide_long_launch_crosses_chunks(D):
     assert_bit_equal(g, r)
 
 
-@pytest.mark.parametrize("D", [72, 300, 1100])
+@pytest.mark.parametrize("D", [48, 72, 300, 1100])
 def test_wide_pipeline_several_blocks_per_workgroup(D):
     """More 256-env blocks than the persistent grid has workgroups (one per CU):
     workgroup 0 runs blocks 0 and 256 one after the other, the last block is
@@ -59,8 +61,9 @@ def test_wide_pipeline_several_blocks_per_workgroup(D):
     of one block pass through the pipeline; a second call of K = 300 follows.
     The columns of blocks 0, 256 and the partial last one -- the trajectory,
     the cart-pole state and every padding word -- and their statistics rows
-    equal the oracle's slices at the same global ids (D = 72, 300 and 1,100 take
-    the 4-, 8- and 32-words-per-lane shapes, of 16, 16 and 12 waves)."""
+    equal the oracle's slices at the same global ids (D = 48, 72, 300 and 1,100
+    take the jump-table, 4-, 8- and 32-words-per-lane shapes, of 16, 16, 16 and
+    12 waves)."""
     n = 256 * 257 + 100
     T, sched = 1100, [800, 300]
     slices = [(0, 256), (256 * 256, 256 * 257), (256 * 257, n)]
@@ -77,7 +80,7 @@ def test_wide_pipeline_several_blocks_per_workgroup(D):
             assert np.array_equal(gs[a // 256:a // 256 + len(rows)], rows), (call, a)
 
 
-@pytest.mark.parametrize("D", [72, 300])
+@pytest.mark.parametrize("D", [48, 300])
 def test_wide_pipeline_without_trajectory(D):
     """The wide kernel's forms without a trajectory, at the multi-block size of
     the test above: a call with traj = NULL and a statistics-only call leave the
