@@ -379,14 +379,14 @@ struct ByteRecorder {
 // 68 i.  A nonzero done byte calls the clearing routine, which zeroes the words
 // of the environments whose bit is set.  The 32 steps are unrolled; a second
 // copy tests the step count m before each step, for a last, partial word.
-// s80..s89 hold the table and routine addresses and the return addresses.
+// s36..s45 hold the table and routine addresses and the return addresses.
 #define JT_M(e) "v_mul_f32_e64 %[s" #e "], %[a" #e "], %[s" #e "]\n"
 #define JT_F(e) "v_fma_f32 %[s" #e "], %[a" #e "], %[s" #e "], %[b" #e "]\n"
 #define JT_OP0(e) JT_M(e)
 #define JT_OP1(e) JT_F(e)
 #define JT_LEAF(b0, b1, b2, b3, b4, b5, b6, b7)                                                            \
     JT_OP##b0(0) JT_OP##b1(1) JT_OP##b2(2) JT_OP##b3(3) JT_OP##b4(4) JT_OP##b5(5) JT_OP##b6(6) JT_OP##b7(7) \
-        "s_setpc_b64 s[88:89]\n"
+        "s_setpc_b64 s[44:45]\n"
 #define JT_T0(b1, b2, b3, b4, b5, b6, b7) JT_LEAF(0, b1, b2, b3, b4, b5, b6, b7) JT_LEAF(1, b1, b2, b3, b4, b5, b6, b7)
 #define JT_T1(b2, b3, b4, b5, b6, b7) JT_T0(0, b2, b3, b4, b5, b6, b7) JT_T0(1, b2, b3, b4, b5, b6, b7)
 #define JT_T2(b3, b4, b5, b6, b7) JT_T1(0, b3, b4, b5, b6, b7) JT_T1(1, b3, b4, b5, b6, b7)
@@ -398,16 +398,16 @@ struct ByteRecorder {
 // one step: leaf call, then the done byte (SCC = byte != 0) and the call of
 // the clearing routine through an out-of-line stub
 #define JT_STEP(P, c, w, bc)                                     \
-    "s_bfe_u32 s84, %[u" #w "], " #bc "\n"                      \
-    "s_mul_i32 s84, s84, 68\n"                                   \
-    "s_add_u32 s86, s80, s84\n"                                  \
-    "s_addc_u32 s87, s81, 0\n"                                   \
-    "s_swappc_b64 s[88:89], s[86:87]\n"                          \
-    "s_bfe_u32 s85, %[d" #w "], " #bc "\n"                      \
+    "s_bfe_u32 s40, %[u" #w "], " #bc "\n"                      \
+    "s_mul_i32 s40, s40, 68\n"                                   \
+    "s_add_u32 s42, s36, s40\n"                                  \
+    "s_addc_u32 s43, s37, 0\n"                                   \
+    "s_swappc_b64 s[44:45], s[42:43]\n"                          \
+    "s_bfe_u32 s41, %[d" #w "], " #bc "\n"                      \
     "s_cbranch_scc1 Lj" #P "c" #c "_%=\n"                        \
     "Lj" #P "r" #c "_%=:\n"
 #define JT_PSTEP(c, w, bc) "s_cmp_le_u32 %[m], " #c "\n s_cbranch_scc1 Ljend%=\n" JT_STEP(p, c, w, bc)
-#define JT_STUB(P, c) "Lj" #P "c" #c "_%=:\n s_swappc_b64 s[88:89], s[82:83]\n s_branch Lj" #P "r" #c "_%=\n"
+#define JT_STUB(P, c) "Lj" #P "c" #c "_%=:\n s_swappc_b64 s[44:45], s[38:39]\n s_branch Lj" #P "r" #c "_%=\n"
 #define JT_WORD(X, P, w, c0, c1, c2, c3) \
     X(P, c0, w, 0x80000) X(P, c1, w, 0x80008) X(P, c2, w, 0x80010) X(P, c3, w, 0x80018)
 #define JT_FSTEP(P, c, w, bc) JT_STEP(P, c, w, bc)
@@ -423,7 +423,7 @@ struct ByteRecorder {
                 JT_STUB(P, 19) JT_STUB(P, 20) JT_STUB(P, 21) JT_STUB(P, 22) JT_STUB(P, 23) JT_STUB(P, 24)  \
                     JT_STUB(P, 25) JT_STUB(P, 26) JT_STUB(P, 27) JT_STUB(P, 28) JT_STUB(P, 29)             \
                         JT_STUB(P, 30) JT_STUB(P, 31)
-#define JT_CLR(e) "s_bitcmp1_b32 s85, " #e "\n s_cbranch_scc0 Ljz" #e "_%=\n v_mov_b32 %[s" #e "], 0\nLjz" #e "_%=:\n"
+#define JT_CLR(e) "s_bitcmp1_b32 s41, " #e "\n s_cbranch_scc0 Ljz" #e "_%=\n v_mov_b32 %[s" #e "], 0\nLjz" #e "_%=:\n"
 #define JT_INA(e) [a##e] "v"(pa[e]),
 #define JT_INB(e) [b##e] "v"(pb[e]),
 #define JT_INU(e) [u##e] "s"(u[e]),
@@ -433,14 +433,14 @@ struct ByteRecorder {
 __device__ __forceinline__ void replay_jt(float (&s)[8], const float (&pa)[8], const float (&pb)[8],
                                           const uint32_t (&u)[8], const uint32_t (&d)[8], uint32_t m)
 {
-    asm volatile("s_getpc_b64 s[80:81]\n"
+    asm volatile("s_getpc_b64 s[36:37]\n"
                  "Ljbase0_%=:\n"
-                 "s_add_u32 s80, s80, Ljtab%= - Ljbase0_%=\n"
-                 "s_addc_u32 s81, s81, 0\n"
-                 "s_getpc_b64 s[82:83]\n"
+                 "s_add_u32 s36, s36, Ljtab%= - Ljbase0_%=\n"
+                 "s_addc_u32 s37, s37, 0\n"
+                 "s_getpc_b64 s[38:39]\n"
                  "Ljbase1_%=:\n"
-                 "s_add_u32 s82, s82, Ljclr%= - Ljbase1_%=\n"
-                 "s_addc_u32 s83, s83, 0\n"
+                 "s_add_u32 s38, s38, Ljclr%= - Ljbase1_%=\n"
+                 "s_addc_u32 s39, s39, 0\n"
                  "s_cmp_eq_u32 %[m], 32\n"
                  "s_cbranch_scc0 Ljpart%=\n"
                  JT_STEPS(JT_FSTEP, f)
@@ -449,32 +449,32 @@ __device__ __forceinline__ void replay_jt(float (&s)[8], const float (&pa)[8], c
                  JT_STEPS(JT_PSTEPX, p)
                  "s_branch Ljend%=\n"
                  JT_STUBS(f) JT_STUBS(p)
-                 "Ljclr%=:\n" JT_R8(JT_CLR) "s_setpc_b64 s[88:89]\n"
+                 "Ljclr%=:\n" JT_R8(JT_CLR) "s_setpc_b64 s[44:45]\n"
                  "Ljtab%=:\n" JT_TABLE
                  "Ljend%=:\n"
                  : [s0] "+v"(s[0]), [s1] "+v"(s[1]), [s2] "+v"(s[2]), [s3] "+v"(s[3]), [s4] "+v"(s[4]),
                    [s5] "+v"(s[5]), [s6] "+v"(s[6]), [s7] "+v"(s[7])
                  : JT_R8(JT_INA) JT_R8(JT_INB) JT_R8(JT_INU) JT_R8(JT_IND)[m] "s"(m)
-                 : "scc", "s80", "s81", "s82", "s83", "s84", "s85", "s86", "s87", "s88", "s89");
+                 : "scc", "s36", "s37", "s38", "s39", "s40", "s41", "s42", "s43", "s44", "s45");
 }
 
 // Phase 2 of group g (columns 8 g .. 8 g + 7 of block blk): lane l holds word
-// l of each of the eight environments.
+// l of each of the eight environments.  Row addresses are recomputed at the
+// store rather than held through the replay (fewer live registers).
 __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t* lds_u, const uint8_t* lds_d,
                                                 uint32_t steps, uint32_t blk, uint32_t g)
 {
     const uint32_t lane = threadIdx.x % 64u;
+    const uint32_t env0 = blk * kBlock + g * kJtGroup;
+    const bool lane_on = lane < a.Dp;
     float s[8], pa[8], pb[8];
-    size_t row[8];
-    bool on[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const uint32_t env = blk * kBlock + g * kJtGroup + (uint32_t)e;
-        row[e] = (size_t)env * a.Dp + lane;
-        on[e] = env < a.n && lane < a.Dp;
-        s[e] = on[e] ? a.pad_s[row[e]] : 0.0f;
-        pa[e] = on[e] ? a.pad_a[row[e]] : 0.0f;
-        pb[e] = on[e] ? a.pad_b[row[e]] : 0.0f;
+        const bool on = lane_on && env0 + (uint32_t)e < a.n;
+        const size_t row = (size_t)(env0 + (uint32_t)e) * a.Dp;
+        s[e] = on ? a.pad_s[row + lane] : 0.0f;
+        pa[e] = on ? a.pad_a[row + lane] : 0.0f;
+        pb[e] = on ? a.pad_b[row + lane] : 0.0f;
     }
     for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
         const uint32_t* pu = reinterpret_cast<const uint32_t*>(lds_u + g * kChunk + w32 * 32u);
@@ -488,8 +488,10 @@ __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t
         replay_jt(s, pa, pb, u, d, __builtin_amdgcn_readfirstlane(min(32u, steps - w32 * 32u)));
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-        if (on[e]) a.pad_s[row[e]] = s[e];
+    for (int e = 0; e < 8; ++e) {
+        const size_t row = (size_t)(env0 + (uint32_t)e) * a.Dp;
+        if (lane_on && env0 + (uint32_t)e < a.n) a.pad_s[row + lane] = s[e];
+    }
 }
 
 // k_cartpole_wide<W, E, NW>: the two phases, overlapped across the blocks of a
@@ -506,8 +508,14 @@ __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t
 // workgroups: D = 512 2.11 against 2.45 ms, D = 2,048 6.33 against 8.59 ms).
 // Block statistics go through LDS slot m & 1 of the workgroup's m-th block and
 // are written out by wave 4 in the iteration after the block's last item.
+// With one word per lane (the jump-table replay, bound by the latency of its
+// jumps rather than by issue) two workgroups run per CU, eight waves per SIMD:
+// D = 64 0.88-0.93 against 0.99-1.05 ms with one.  There the stepping waves
+// join the replay only after the workgroup's last item, which keeps the kernel
+// within the 64 VGPRs that eight waves per SIMD allow, without spills.
 template <int W, int E, int NW, bool REC, bool STATS>
-__global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W == 1 ? 8 : 1)))
+void k_cartpole_wide(StepArgs a)
 {
     static_assert(NW >= 8 && NW <= 16, "the pipeline needs four stepping waves and at least four more");
     static_assert(W != 1 || E == (int)kJtGroup, "one word per lane takes the eight-environment jump table");
@@ -591,7 +599,11 @@ __global__ __launch_bounds__(64 * NW) void k_cartpole_wide(StepArgs a)
                         }
                     }
                 }
-                if (j >= 1u) replay_item(j - 1u);
+                // with one word per lane the stepping waves join the replay only
+                // after their last item: their cart-pole state and the replay's
+                // words then never share registers, which keeps the kernel at
+                // eight waves per SIMD, two workgroups per CU, without spills
+                if (W != 1 && j >= 1u) replay_item(j - 1u);
                 __syncthreads();
             }
         }

@@ -204,10 +204,10 @@ unsigned grid_for(uint32_t n) { return (n + kBlock - 1u) / kBlock; }
 
 // Largest padding count of the register-resident (one thread per env) kernel;
 // above it the two-phase wide kernel holds the words.  (262,144 envs x 500
-// steps: D = 32 0.82-0.87 ms in registers against 1.01-1.03 ms for the wide
-// kernel's eight-environment jump table, one word per lane, whose cost does not
-// shrink with D; D = 48 and 64 1.07-1.13 ms in registers, where every thread
-// updates all 64 words, against 0.99-1.03 ms.)
+// steps: D = 32 0.82-0.87 ms in registers; the wide kernel's eight-environment
+// jump table, one word per lane, costs the same at every D up to 64, 0.88-0.94 ms
+// at D = 48 and 64, where the register form, every thread updating all 64 words,
+// takes 1.07-1.13 ms.)
 constexpr uint32_t kMaxRegisterWords = 32u;
 // Fewest steps per call for which a trajectory-recording call runs the
 // warp-specialised kernel: without padding words, and with 1-4 padding words.
@@ -244,11 +244,14 @@ hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s
         // E = 2 5.0 against E = 1 3.94 ms: four environments of 8 words, or two
         // of 16, take the kernel past 128 VGPRs and below four waves per SIMD).
         // Up to 64 words: one word per lane, eight environments per step
-        // through the replay's jump table.  One persistent workgroup per CU, of
+        // through the replay's jump table, two workgroups per CU.  Otherwise
+        // one persistent workgroup per CU, of
         // as many waves as the replay's registers allow four of per SIMD (three
         // for W = 32, two for W = 64).
         const dim3 pgrid(min(grid_for(a.n), cus));
-        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
+        if (a.D <= 64u)
+            hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), dim3(min(grid_for(a.n), 2u * cus)), dim3(1024), 0,
+                               s, a);
         else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);

@@ -39,7 +39,7 @@ def test_jump_tables_have_the_layout_the_replay_jumps_into(tmp_path):
     tables = {k[len("Ljtab"):]: v for k, v in labels.items() if k.startswith("Ljtab")}
     assert tables, "no jump table in the built library"
     for uid, base in tables.items():
-        for lab, reg, target in (("Ljbase0_", "s80", base), ("Ljbase1_", "s82", labels["Ljclr" + uid])):
+        for lab, reg, target in (("Ljbase0_", "s36", base), ("Ljbase1_", "s38", labels["Ljclr" + uid])):
             start = labels[lab + uid]
             m = re.match(rf"s_add_u32 {reg}, {reg}, (0x[0-9a-f]+|\d+)$", ins[at[start]][1])
             assert m and start + int(m.group(1), 0) == target, (uid, lab, ins[at[start]])
@@ -51,10 +51,10 @@ def test_jump_tables_have_the_layout_the_replay_jumps_into(tmp_path):
                 want = "v_fma_f32 " if (leaf >> e) & 1 else "v_mul_f32_e64 "
                 assert text.startswith(want) and size == 8, (uid, leaf, e, text, size)
                 k += 1
-            assert ins[k][1] == "s_setpc_b64 s[88:89]" and ins[k][2] == 4, (uid, leaf, ins[k])
+            assert ins[k][1] == "s_setpc_b64 s[44:45]" and ins[k][2] == 4, (uid, leaf, ins[k])
             k += 1
-    muls = {t for _, t, _ in ins if re.match(r"s_mul_i32 s84, s84,", t)}
-    assert muls == {f"s_mul_i32 s84, s84, {LEAF_BYTES:#x}"}, muls
+    muls = {t for _, t, _ in ins if re.match(r"s_mul_i32 s40, s40,", t)}
+    assert muls == {f"s_mul_i32 s40, s40, {LEAF_BYTES:#x}"}, muls
     # every step's call, and every stub's call of the clearing routine, as many as the tables need
-    calls = [t for _, t, _ in ins if t.startswith("s_swappc_b64 s[88:89], ")]
+    calls = [t for _, t, _ in ins if t.startswith("s_swappc_b64 s[44:45], ")]
     assert len(calls) == len(tables) * 4 * 32, (len(calls), len(tables))
