@@ -454,59 +454,81 @@ def stream_ceiling(words: int, achieved_gbs: float, stream) -> dict:
 
 
 # iterations per launch of each instruction-rate probe kind (about 1-3 ms)
-ISSUE_ITERS = {"fma": 16384, "select_fma": 8192, "exp": 4096, "rcp": 4096, "mfma": 1024, "mixed": 1024, "mul": 16384}
+ISSUE_ITERS = {"fma": 16384, "fma_shared": 16384, "select_fma": 8192, "exp": 4096, "rcp": 4096, "mfma": 1024,
+               "mixed": 1024, "mul": 16384, "replay_tree": 256, "replay_flat": 256}
 CUS = 256
+SIMDS = 4 * CUS
 
 
-def _probe_ms(kind: str, waves: int, iters: int, out, stream, reps: int = 5) -> float:
+def _probe_ms(kind: str, waves: int, iters: int, out, stream, reps: int = 5, clocks=None):
+    """Median launch time of probe `kind` over `reps` launches; with `clocks`,
+    also the median shader clock (GHz) of the last launch's workgroups."""
     import torch
-    from paper_2207_07736_amd.probe import probe_issue
+    from paper_2207_07736_amd.probe import probe_issue, wall_clock_khz
     blocks = CUS * waves
     probe_issue(kind, blocks, iters, out, stream)
     times = []
     for _ in range(reps):
         start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         start.record(stream)
-        probe_issue(kind, blocks, iters, out, stream)
+        probe_issue(kind, blocks, iters, out, stream, clocks=clocks)
         stop.record(stream)
         torch.cuda.synchronize()
         times.append(start.elapsed_time(stop))
     times.sort()
-    return times[len(times) // 2]
+    ms = times[len(times) // 2]
+    if clocks is None:
+        return ms
+    c = clocks[:2 * blocks].view(blocks, 2).double().cpu()
+    ghz = float((c[:, 0] / c[:, 1]).median()) * wall_clock_khz() * 1e-6
+    return ms, ghz
 
 
 def issue_rates(stream) -> dict:
     """The instruction rates the kernels' bounds rest on (rlsim_probe_issue),
-    with `waves` waves per SIMD (256 CUs x 4 SIMDs): wave64 v_fma_f32 as fp32
-    lane operations per second, and v_mul_f32 likewise; the per-lane padding update (a select and an
-    FMA per word) as word updates per second; v_exp_f32 and v_rcp_f32 as
-    lanes per second; fp32 MFMA as TFLOP/s; and one MFMA wave beside one FMA
+    with `waves` waves per SIMD (256 CUs x 4 SIMDs): wave64 v_fma_f32 (with
+    distinct source registers, and with one register read twice), v_mul_f32,
+    v_exp_f32 and v_rcp_f32 as fp32 lane operations per second; the per-lane
+    padding update (a select and an FMA per word) and the wide kernel's
+    two-environment replay, with its scalar decisions and with none, as word
+    updates per second; fp32 MFMA as TFLOP/s; and one MFMA wave beside one FMA
     wave on every SIMD against each alone (serialised if the mixed time is the
-    sum of the two)."""
+    sum of the two).  Each rate also comes per clock, as lanes per cycle per
+    SIMD at the shader clock the probe's own workgroups counted: the clock
+    follows the power draw, so rates per second differ with the data."""
     import torch
     out = torch.empty(CUS * 8 * 256, dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(CUS * 8 * 2, dtype=torch.int64, device="cuda")
     res = {}
-    for kind, waves in (("fma", 1), ("fma", 2), ("fma", 4), ("fma", 8), ("mul", 8), ("select_fma", 2),
-                        ("select_fma", 8), ("exp", 8), ("rcp", 8)):
+    for kind, waves in (("fma", 1), ("fma", 2), ("fma", 4), ("fma", 8), ("fma_shared", 8), ("mul", 8),
+                        ("select_fma", 2), ("select_fma", 8), ("exp", 8), ("rcp", 8), ("replay_tree", 4),
+                        ("replay_tree", 8), ("replay_flat", 4), ("replay_flat", 8)):
         it = ISSUE_ITERS[kind]
-        ms = _probe_ms(kind, waves, it, out, stream)
-        lanes = CUS * waves * 256 * it * 8
-        res[f"{kind}_w{waves}"] = {"ms": ms, "per_s": lanes / (ms * 1e-3),
-                                   "unit": "word updates" if kind == "select_fma" else "lane ops"}
+        ms, ghz = _probe_ms(kind, waves, it, out, stream, clocks=clocks)
+        if kind.startswith("replay"):
+            lanes, unit = CUS * waves * 256 * it * 32 * 16, "word updates"
+        else:
+            lanes, unit = CUS * waves * 256 * it * 8, "word updates" if kind == "select_fma" else "lane ops"
+        per_s = lanes / (ms * 1e-3)
+        res[f"{kind}_w{waves}"] = {"ms": ms, "per_s": per_s, "unit": unit, "clock_ghz": ghz,
+                                   "lanes_per_clk_per_simd": per_s / (SIMDS * ghz * 1e9)}
     it = ISSUE_ITERS["mfma"]
     for waves in (1, 2):
-        ms = _probe_ms("mfma", waves, it, out, stream)
+        ms, ghz = _probe_ms("mfma", waves, it, out, stream, clocks=clocks)
         flops = CUS * waves * 4 * it * 4 * (32 * 32 * 2 * 2)
-        res[f"mfma_f32_w{waves}"] = {"ms": ms, "TFLOPs": flops / (ms * 1e-3) / 1e12}
+        res[f"mfma_f32_w{waves}"] = {"ms": ms, "TFLOPs": flops / (ms * 1e-3) / 1e12, "clock_ghz": ghz,
+                                     "flops_per_clk_per_cu": flops / (ms * 1e-3) / (CUS * ghz * 1e9)}
     # one MFMA wave and one FMA wave per SIMD, against each alone at one wave per SIMD
     mixed = _probe_ms("mixed", 2, it, out, stream)
     fma_alone = _probe_ms("fma", 1, 16 * it, out, stream)
     res["mfma_beside_fma"] = {"mixed_ms": mixed, "mfma_alone_ms": res["mfma_f32_w1"]["ms"], "fma_alone_ms": fma_alone,
                               "mixed_over_sum": mixed / (res["mfma_f32_w1"]["ms"] + fma_alone),
                               "mixed_over_max": mixed / max(res["mfma_f32_w1"]["ms"], fma_alone)}
-    del out
-    print("[bench] issue rates: " + ", ".join(f"{k} {v.get('per_s', v.get('TFLOPs', v.get('mixed_over_sum'))):.3g}"
-                                             for k, v in res.items()), file=sys.stderr, flush=True)
+    del out, clocks
+    print("[bench] issue rates: " + ", ".join(
+        f"{k} {v.get('per_s', v.get('TFLOPs', v.get('mixed_over_sum'))):.3g}"
+        + (f" ({v['lanes_per_clk_per_simd']:.1f}/clk at {v['clock_ghz']:.2f} GHz)" if "lanes_per_clk_per_simd" in v else "")
+        for k, v in res.items()), file=sys.stderr, flush=True)
     return res
 
 

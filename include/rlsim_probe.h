@@ -75,22 +75,48 @@ int rlsim_probe_stream(uint64_t n4, float* s, const float* a, const float* b, vo
  * one wave on each SIMD of a 256-CU device, 256 w blocks w waves), each lane
  * running `iters` iterations of eight independent chains (MFMA: four) of one
  * instruction kind:
- *   kind 0  v_fma_f32 x <- x * 1 + 1, x0 = lane + j       -> x0 + iters
+ *   kind 0  v_fma_f32 x <- x * 1 + 1, the two 1s in two registers,
+ *           x0 = lane + j                                  -> x0 + iters
  *   kind 1  the per-lane padding update t <- u ? 1 : -0, s <- fma(1, s, t),
  *           u = (lane + i) odd, s0 = j                     -> s0 + #odd steps
  *   kind 2  v_exp_f32 x <- 2^-x                            -> the root of x = 2^-x
  *   kind 3  v_rcp_f32 x <- 1 / x, x0 = 2^j                 -> x0 (even iters)
  *   kind 4  v_mfma_f32_32x32x2_f32 C <- A B + C, A = B = 1 -> 2 iters per element
- *   kind 5  kind 4 with `iters` and kind 0 with 16 iters (about as long) in
- *           alternate waves (workgroup b, wave w: MFMA when b + w is even), so
- *           that both share each SIMD
+ *   kind 5  kind 4 with `iters` and kind 0 with 16 iters in alternate waves
+ *           (workgroup b, wave w: MFMA when b + w is even), so that both
+ *           share each SIMD
  *   kind 6  v_mul_f32 x <- x * 1, x0 = lane + j            -> x0
+ *   kind 7  kind 0 with both 1s read from one register     -> x0 + iters
+ *   kind 8  the wide kernel's padding replay of two environments, 8 words per
+ *           lane each (per step a tree of scalar bit tests, then 16 in-place
+ *           v_fma_f32 / v_mul_f32), over `iters` 32-step bit words; a = b = 1,
+ *           so each word ends as the count of action-1 steps since its
+ *           environment's last done bit.  The bits of word w of global wave g
+ *           (g = 4 blockIdx + wave) come from hash(4k), hash(4k + 1) and
+ *           hash(4k + 2), k = g iters + w (hash: x ^= x >> 16, x *= 0x7feb352d,
+ *           x ^= x >> 15, x *= 0x846ca68b, x ^= x >> 16 on uint32): action words
+ *           u0 = hash(4k), u1 = hash(4k + 1); with h = hash(4k + 2), done words
+ *           d0 = 1 << (h & 31) | (((h >> 5) mod 3 == 0) << ((h >> 8) & 31)),
+ *           d1 = 1 << ((h >> 13) & 31) | (((h >> 18) mod 3 == 0) << ((h >> 21) & 31))
+ *   kind 9  the same 16 updates per step with no decisions: every 8 steps,
+ *           environment 0 takes the FMA at steps 0, 3, 4, 5 and environment 1
+ *           at the others                                  -> 16 iters per word
  * out (caller-owned DEVICE, blocks * 256 floats) receives per thread the sum
- * of its chains' final values (kinds 0-3: over j = 0..7; MFMA: elements 0, 5,
- * 10, 15 of the four accumulators, 8 iters).  The caller times the launch.
- * Errors: -1 if kind > 6, blocks == 0 or > 2^20, iters == 0 or > 2^22 (kind
- * 5: > 2^19), or out is NULL or not 4-byte aligned; -3 if the launch fails. */
-int rlsim_probe_issue(uint32_t kind, uint32_t blocks, uint32_t iters, float* out, void* stream);
+ * of its chains' final values (kinds 0-3, 6, 7: over j = 0..7; MFMA: elements
+ * 0, 5, 10, 15 of the four accumulators, 8 iters; kinds 8, 9: over both
+ * environments' 8 words).  clocks (caller-owned DEVICE, 2 blocks uint64, or
+ * NULL) receives per workgroup the shader-clock cycles (s_memtime) and the
+ * real-time ticks (s_memrealtime, at rlsim_probe_wall_clock_khz) that its
+ * thread 0 took over its chains.  The caller times the launch.
+ * Errors: -1 if kind > 9, blocks == 0 or > 2^20, iters == 0 or > 2^22 (kind
+ * 5: > 2^19; kinds 8, 9: > 2^16), or out is NULL or not 4-byte aligned, or
+ * clocks is not 8-byte aligned; -3 if the launch fails. */
+int rlsim_probe_issue(uint32_t kind, uint32_t blocks, uint32_t iters, float* out, uint64_t* clocks, void* stream);
+
+/* Frequency of the real-time counter that rlsim_probe_issue's clocks count in,
+ * in kHz, for the current device, into *khz.  Errors: -1 if khz is NULL; -3 if
+ * the device query fails. */
+int rlsim_probe_wall_clock_khz(uint32_t* khz);
 
 /* Store-rate probe of kernel shape (section "Simulator Kernel Fusion": what a
  * fused kernel's trajectory stores can reach depends on how they are issued):

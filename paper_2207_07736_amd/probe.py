@@ -12,8 +12,8 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "librlsim_probe.so")
 PROBE_EXPORTS = ("rlsim_probe_store", "rlsim_probe_policy_math", "rlsim_probe_stream", "rlsim_probe_issue",
-                 "rlsim_probe_fill")
-ISSUE_KINDS = ("fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul")
+                 "rlsim_probe_wall_clock_khz", "rlsim_probe_fill")
+ISSUE_KINDS = ("fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul", "fma_shared", "replay_tree", "replay_flat")
 
 
 def _load():
@@ -27,8 +27,10 @@ def _load():
     L.rlsim_probe_policy_math.restype = ctypes.c_int
     L.rlsim_probe_stream.argtypes = [ctypes.c_uint64, vp, vp, vp, vp]
     L.rlsim_probe_stream.restype = ctypes.c_int
-    L.rlsim_probe_issue.argtypes = [u32, u32, u32, vp, vp]
+    L.rlsim_probe_issue.argtypes = [u32, u32, u32, vp, vp, vp]
     L.rlsim_probe_issue.restype = ctypes.c_int
+    L.rlsim_probe_wall_clock_khz.argtypes = [ctypes.POINTER(u32)]
+    L.rlsim_probe_wall_clock_khz.restype = ctypes.c_int
     L.rlsim_probe_fill.argtypes = [ctypes.c_uint64, u32, vp, vp]
     L.rlsim_probe_fill.restype = ctypes.c_int
     return L
@@ -71,17 +73,30 @@ def probe_stream(s, a, b, stream=None) -> None:
         raise ValueError(f"rlsim_probe_stream rejected its arguments (status {rc})")
 
 
-def probe_issue(kind: str, blocks: int, iters: int, out, stream=None) -> None:
+def probe_issue(kind: str, blocks: int, iters: int, out, stream=None, clocks=None) -> None:
     """Run the instruction-rate probe `kind` (one of ISSUE_KINDS) over `blocks`
     workgroups of 256 threads, `iters` iterations each, results into out (a
-    float32 device tensor of blocks * 256); raises ValueError on a rejected
-    argument."""
+    float32 device tensor of blocks * 256) and, if given, each workgroup's
+    shader cycles and real-time ticks into clocks (an int64 device tensor of
+    blocks * 2); raises ValueError on a rejected argument."""
     if out.numel() < blocks * 256:
         raise ValueError("out must hold blocks * 256 floats")
+    if clocks is not None and clocks.numel() < 2 * blocks:
+        raise ValueError("clocks must hold 2 * blocks values")
     st = None if stream is None else (stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
-    rc = probe_lib.rlsim_probe_issue(ISSUE_KINDS.index(kind), int(blocks), int(iters), _ptr(out), st)
+    rc = probe_lib.rlsim_probe_issue(ISSUE_KINDS.index(kind), int(blocks), int(iters), _ptr(out),
+                                     None if clocks is None else _ptr(clocks), st)
     if rc != 0:
         raise ValueError(f"rlsim_probe_issue rejected its arguments (status {rc})")
+
+
+def wall_clock_khz() -> int:
+    """Frequency of the counter behind probe_issue's real-time ticks, in kHz."""
+    khz = ctypes.c_uint32(0)
+    rc = probe_lib.rlsim_probe_wall_clock_khz(ctypes.byref(khz))
+    if rc != 0:
+        raise RuntimeError(f"rlsim_probe_wall_clock_khz failed (status {rc})")
+    return int(khz.value)
 
 
 def probe_fill(dst, per_thread: int, stream=None) -> None:

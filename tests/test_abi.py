@@ -208,12 +208,16 @@ def test_probe_library_exports_and_rejects_bad_arguments():
     assert L.rlsim_probe_stream(0, 16, 16, 16, None) == -1
     assert L.rlsim_probe_stream(4, None, 16, 16, None) == -1
     assert L.rlsim_probe_stream(4, 16, 24, 16, None) == -1          # misaligned a
-    assert L.rlsim_probe_issue(7, 1, 1, 16, None) == -1               # unknown kind
-    assert L.rlsim_probe_issue(0, 0, 1, 16, None) == -1
-    assert L.rlsim_probe_issue(0, 1, 0, 16, None) == -1
-    assert L.rlsim_probe_issue(5, 1, (1 << 19) + 1, 16, None) == -1
-    assert L.rlsim_probe_issue(0, 1, 1, None, None) == -1
-    assert L.rlsim_probe_issue(0, 1, 1, 18, None) == -1               # misaligned out
+    assert L.rlsim_probe_issue(10, 1, 1, 16, None, None) == -1         # unknown kind
+    assert L.rlsim_probe_issue(0, 0, 1, 16, None, None) == -1
+    assert L.rlsim_probe_issue(0, 1, 0, 16, None, None) == -1
+    assert L.rlsim_probe_issue(5, 1, (1 << 19) + 1, 16, None, None) == -1
+    assert L.rlsim_probe_issue(8, 1, (1 << 16) + 1, 16, None, None) == -1
+    assert L.rlsim_probe_issue(9, 1, (1 << 16) + 1, 16, None, None) == -1
+    assert L.rlsim_probe_issue(0, 1, 1, None, None, None) == -1
+    assert L.rlsim_probe_issue(0, 1, 1, 18, None, None) == -1         # misaligned out
+    assert L.rlsim_probe_issue(0, 1, 1, 16, 20, None) == -1           # misaligned clocks
+    assert L.rlsim_probe_wall_clock_khz(None) == -1
     assert L.rlsim_probe_fill(0, 1, 16, None) == -1
     assert L.rlsim_probe_fill(16, 0, 16, None) == -1
     assert L.rlsim_probe_fill(16, (1 << 20) + 1, 16, None) == -1

@@ -94,24 +94,65 @@ def test_fill_probe_values(per):
     assert np.all(got[4 * n4:] == -7.0)
 
 
-@pytest.mark.parametrize("kind", ["fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul"])
+def _hash32(x: int) -> int:
+    m = 0xFFFFFFFF
+    x ^= x >> 16
+    x = (x * 0x7FEB352D) & m
+    x ^= x >> 15
+    x = (x * 0x846CA68B) & m
+    x ^= x >> 16
+    return x
+
+
+def _replay_tree_want(blocks: int, iters: int):
+    """Closed form of the replay kind: per wave, 8 x (the count of action-1
+    steps since each environment's last done bit), from the bit recipe of
+    include/rlsim_probe.h."""
+    import numpy as np
+    want = np.zeros((blocks, 4, 64))
+    for g in range(blocks * 4):
+        cnt = [0, 0]
+        for w in range(iters):
+            k = (g * iters + w) & 0xFFFFFFFF
+            u = [_hash32((4 * k) & 0xFFFFFFFF), _hash32((4 * k + 1) & 0xFFFFFFFF)]
+            h = _hash32((4 * k + 2) & 0xFFFFFFFF)
+            d = [(1 << (h & 31)) | ((1 << ((h >> 8) & 31)) if (h >> 5) % 3 == 0 else 0),
+                 (1 << ((h >> 13) & 31)) | ((1 << ((h >> 21) & 31)) if (h >> 18) % 3 == 0 else 0)]
+            for t in range(32):
+                for e in range(2):
+                    if (u[e] >> t) & 1:
+                        cnt[e] += 1
+                    if (d[e] >> t) & 1:
+                        cnt[e] = 0
+        want[g // 4, g % 4, :] = 8 * (cnt[0] + cnt[1])
+    return want
+
+
+@pytest.mark.parametrize("kind", ["fma", "select_fma", "exp", "rcp", "mfma", "mixed", "mul", "fma_shared",
+                                  "replay_tree", "replay_flat"])
 def test_issue_probe_values(kind):
     """rlsim_probe_issue runs the instruction chains it claims: every thread's
     sum of chain results equals the closed form of its kind (exact integers for
-    the FMA, select and MFMA chains and the rcp cycle; the fixed point of
-    x = 2^-x for exp, to the hardware exp2's accuracy)."""
+    the FMA, select, MFMA and replay chains and the rcp cycle; the fixed point
+    of x = 2^-x for exp, to the hardware exp2's accuracy), and each
+    workgroup's clock record puts its shader clock between 0.3 and 3.5 GHz."""
     import math
 
     import numpy as np
-    from paper_2207_07736_amd.probe import probe_issue
+    from paper_2207_07736_amd.probe import probe_issue, wall_clock_khz
     blocks, iters = 3, 101
     out = torch.full((blocks * 256,), float("nan"), dtype=torch.float32, device="cuda")
-    probe_issue(kind, blocks, iters, out)
+    clocks = torch.zeros(2 * blocks, dtype=torch.int64, device="cuda")
+    probe_issue(kind, blocks, iters, out, clocks=clocks)
     torch.cuda.synchronize()
+    c = clocks.cpu().numpy().reshape(blocks, 2)
+    assert np.all(c > 0)
+    ghz = c[:, 0] / c[:, 1] * wall_clock_khz() * 1e-6
+    assert np.all((ghz > 0.3) & (ghz < 3.5)), ghz
     got = out.cpu().numpy().reshape(blocks, 4, 64)
     lane = np.arange(64)
     fma = np.sum([lane + j + iters for j in range(8)], axis=0).astype(np.float64)
-    if kind == "fma":
+    if kind in ("fma", "fma_shared"):
         want = np.broadcast_to(fma, got.shape)
     elif kind == "mul":
         want = np.broadcast_to(np.sum([lane + j for j in range(8)], axis=0).astype(np.float64), got.shape)
@@ -122,6 +163,11 @@ def test_issue_probe_values(kind):
         want = np.full(got.shape, sum(2.0**-j for j in range(8)))          # odd iteration count: reciprocals
     elif kind == "mfma":
         want = np.full(got.shape, 8.0 * iters)
+    elif kind == "replay_tree":
+        want = _replay_tree_want(blocks, iters)
+        assert np.any(want != want.flat[0])                             # the bits differ between waves
+    elif kind == "replay_flat":
+        want = np.full(got.shape, 8.0 * 32 * iters)
     elif kind == "mixed":
         b = np.arange(blocks)[:, None, None]
         w = np.arange(4)[None, :, None]
@@ -141,7 +187,8 @@ def test_issue_probe_values(kind):
 def test_issue_probe_rejects_bad_arguments():
     from paper_2207_07736_amd.probe import probe_issue
     out = torch.zeros(256, dtype=torch.float32, device="cuda")
-    for kind, blocks, iters in (("fma", 0, 1), ("fma", 1, 0), ("mixed", 1, (1 << 19) + 1), ("fma", 1, (1 << 22) + 1)):
+    for kind, blocks, iters in (("fma", 0, 1), ("fma", 1, 0), ("mixed", 1, (1 << 19) + 1), ("fma", 1, (1 << 22) + 1),
+                                ("replay_tree", 1, (1 << 16) + 1)):
         with pytest.raises(ValueError):
             probe_issue(kind, blocks, iters, out)
     with pytest.raises(ValueError):
