@@ -22,13 +22,28 @@ constexpr uint32_t kChunkWords = kChunk / 32u;   // 32-bit bit words per env per
 
 // Phase-1 hook: collects each step's action and done bits, 32 steps per word,
 // into this thread's LDS columns.
+// Episode ends of one environment within one round of at most kChunk = 512
+// steps, three 10-bit counts in one register: episodes ended (bits 0-9),
+// terminated (10-19) and truncated (20-29).  The done byte d is term + 2 trunc.
+template <bool STATS>
+struct RoundCounts {
+    uint32_t packed = 0u;
+    __device__ __forceinline__ void add(uint32_t d)
+    {
+        if (STATS) packed += min(d, 1u) | ((d & 1u) << 10) | ((d & 2u) << 19);
+    }
+};
+static_assert(kChunk < 1024u, "the per-round episode counts are 10-bit fields");
+
+template <bool STATS>
 struct BitRecorder {
     uint32_t* lds_u;     // [kChunkWords][kBlock]
     uint32_t* lds_d;
     uint32_t col;        // threadIdx.x
     uint32_t k = 0u;     // step index within the round
     uint32_t ub = 0u, db = 0u;
-    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
+    RoundCounts<STATS> cnt{};
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t d) { cnt.add(d); }
     __device__ __forceinline__ void operator()(uint32_t act, bool reset)
     {
         const uint32_t bit = k & 31u;
@@ -231,6 +246,17 @@ __device__ __forceinline__ void replay_multi(float (&s0)[W], float (&s1)[W], flo
     (void)s2; (void)s3; (void)a2; (void)a3; (void)b2; (void)b3;
 }
 
+// A buffer resource over one environment's row of Dp padding words (none for
+// an environment past n): loads outside it read 0 and stores outside it are
+// dropped by the hardware's range check, so a wave-uniform resource and the
+// lane's byte offset address every word, with no per-lane bounds test.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const float* row, uint32_t words)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), (short)0, (int)(words * 4u), 0x00020000);
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // E environments replayed together (columns col0 .. col0 + E - 1 of block
 // blk): W words per lane per environment, loaded as float4 with the placement
 // of replay_env.
@@ -250,22 +276,37 @@ __device__ __forceinline__ void replay_group(const StepArgs& a, const uint32_t* 
         env[e] = blk * kBlock + col[e];
         live[e] = e < E && env[e] < a.n;
     }
+    // wave-uniform buffer resources over the E rows (scalar registers): each
+    // load and store needs only the lane's byte offset in a VGPR
+    __amdgpu_buffer_rsrc_t rs[4], ra[4], rb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const size_t row = (size_t)env[e] * a.Dp;
+        const uint32_t words = live[e] ? a.Dp : 0u;
+        rs[e] = row_rsrc(a.pad_s + row, words);
+        ra[e] = row_rsrc(a.pad_a + row, words);
+        rb[e] = row_rsrc(a.pad_b + row, words);
+    }
     for (uint32_t c = 0; c < n_chunks; ++c) {
         const uint32_t base = c * chunk_words + 4u * lane;
         float s[4][W], pa[4][W], pb[4][W];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const size_t row = (size_t)env[e] * a.Dp;
 #pragma unroll
             for (int i = 0; i < W; i += 4) {
-                const uint32_t j = base + (uint32_t)(i / 4) * 256u;
-                const bool on = live[e] && j < a.Dp;
-                const float4 vs = on ? *reinterpret_cast<const float4*>(a.pad_s + row + j) : float4{0, 0, 0, 0};
-                const float4 va = on ? *reinterpret_cast<const float4*>(a.pad_a + row + j) : float4{0, 0, 0, 0};
-                const float4 vb = on ? *reinterpret_cast<const float4*>(a.pad_b + row + j) : float4{0, 0, 0, 0};
-                s[e][i] = vs.x; s[e][i + 1] = vs.y; s[e][i + 2] = vs.z; s[e][i + 3] = vs.w;
-                pa[e][i] = va.x; pa[e][i + 1] = va.y; pa[e][i + 2] = va.z; pa[e][i + 3] = va.w;
-                pb[e][i] = vb.x; pb[e][i + 1] = vb.y; pb[e][i + 2] = vb.z; pb[e][i + 3] = vb.w;
+                const uint32_t jb = 4u * (base + (uint32_t)(i / 4) * 256u);
+                u32x4 vs = {0u, 0u, 0u, 0u}, va = vs, vb = vs;
+                if (e < E) {
+                    vs = __builtin_amdgcn_raw_buffer_load_b128(rs[e], jb, 0, 0);
+                    va = __builtin_amdgcn_raw_buffer_load_b128(ra[e], jb, 0, 0);
+                    vb = __builtin_amdgcn_raw_buffer_load_b128(rb[e], jb, 0, 0);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    s[e][i + q] = __uint_as_float(vs[q]);
+                    pa[e][i + q] = __uint_as_float(va[q]);
+                    pb[e][i + q] = __uint_as_float(vb[q]);
+                }
             }
         }
         for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
@@ -280,13 +321,13 @@ __device__ __forceinline__ void replay_group(const StepArgs& a, const uint32_t* 
                                db, m);
         }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const size_t row = (size_t)env[e] * a.Dp;
+        for (int e = 0; e < E; ++e) {
 #pragma unroll
             for (int i = 0; i < W; i += 4) {
-                const uint32_t j = base + (uint32_t)(i / 4) * 256u;
-                if (live[e] && j < a.Dp)
-                    *reinterpret_cast<float4*>(a.pad_s + row + j) = float4{s[e][i], s[e][i + 1], s[e][i + 2], s[e][i + 3]};
+                const uint32_t jb = 4u * (base + (uint32_t)(i / 4) * 256u);
+                const u32x4 v = {__float_as_uint(s[e][i]), __float_as_uint(s[e][i + 1]), __float_as_uint(s[e][i + 2]),
+                                 __float_as_uint(s[e][i + 3])};
+                __builtin_amdgcn_raw_buffer_store_b128(v, rs[e], jb, 0, 0);
             }
         }
     }
@@ -350,12 +391,14 @@ constexpr uint32_t kJtGroup = 8;                     // environments per replay 
 // the wave -- in LDS rows [group][step].  Lane g of a wave writes its group's
 // bytes; a group with a live environment has a live writer (environments past n
 // are the wave's last lanes).
+template <bool STATS>
 struct ByteRecorder {
     uint8_t* lds_u;      // [kBlock / kJtGroup][kChunk]
     uint8_t* lds_d;
     uint32_t lane, wave;
     uint32_t k = 0u;     // step index within the round
-    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t) {}
+    RoundCounts<STATS> cnt{};
+    __device__ __forceinline__ void record(const CartState&, uint32_t, uint32_t d) { cnt.add(d); }
     __device__ __forceinline__ void operator()(uint32_t act, bool reset)
     {
         const uint64_t ub = __builtin_amdgcn_ballot_w64(act != 0u);
@@ -514,7 +557,7 @@ __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t
 // join the replay only after the workgroup's last item, which keeps the kernel
 // within the 64 VGPRs that eight waves per SIMD allow, without spills.
 template <int W, int E, int NW, bool REC, bool STATS>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W == 1 ? 8 : 1)))
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W <= 8 ? 8 : 1)))
 void k_cartpole_wide(StepArgs a)
 {
     static_assert(NW >= 8 && NW <= 16, "the pipeline needs four stepping waves and at least four more");
@@ -539,7 +582,10 @@ void k_cartpole_wide(StepArgs a)
     // from the counter of slot i & 1 until none is left
     auto replay_item = [&](uint32_t i) {
         const uint32_t m = i / rounds, r = i % rounds;
-        const uint32_t blk = wg + m * G;
+        // wave-uniform by construction; readfirstlane keeps the compiler from
+        // merging it with the same sum computed under the statistics' lane test,
+        // which would make it, and every row address after it, per-lane
+        const uint32_t blk = __builtin_amdgcn_readfirstlane(wg + m * G);
         const uint32_t k0 = r * kChunk, steps = min(kChunk, a.K - k0);
         const uint32_t cols = min((uint32_t)kBlock, a.n - blk * kBlock);
         const uint32_t n_groups = (cols + (uint32_t)E - 1u) / (uint32_t)E;
@@ -566,44 +612,58 @@ void k_cartpole_wide(StepArgs a)
             const uint32_t blk = wg + m * G;
             const uint32_t env = blk * kBlock + col;
             const bool live = env < a.n;
-            CartCore<REC, STATS> core(a.p, env);
+            // the episode counts go through the recorder and LDS, not the core,
+            // which keeps them out of the stepping loop's registers
+            CartCore<REC, false> core(a.p, env);
             if (live) core.load(a);
+            if (STATS) {
+                // the block's finished episode lengths: the episode counters at the
+                // start plus K per environment, minus the counters at the end
+                const uint32_t e0 = wave_sum(live ? core.ep : 0u);
+                const uint32_t nl = (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(live));
+                if (lane == 0u) atomicAdd(&blk_stats[m & 1u][1], e0 + nl * a.K);
+            }
             for (uint32_t r = 0; r < rounds; ++r, ++j) {
                 const uint32_t k0 = r * kChunk, steps = min(kChunk, a.K - k0);
                 // slot j & 1's counter was last used in iteration j - 1
                 if (threadIdx.x == 0u) next_group[j & 1u] = 0u;
+                uint32_t counts = 0u;
                 if (live) {
                     if (REC) core.set_rows(a, k0);
                     if constexpr (W == 1) {
-                        ByteRecorder rec{reinterpret_cast<uint8_t*>(lds_u[j & 1u]),
-                                         reinterpret_cast<uint8_t*>(lds_d[j & 1u]), lane, wave};
+                        ByteRecorder<STATS> rec{reinterpret_cast<uint8_t*>(lds_u[j & 1u]),
+                                                reinterpret_cast<uint8_t*>(lds_d[j & 1u]), lane, wave};
                         core.run(a.t0 + k0, steps, rec);
+                        counts = rec.cnt.packed;
                     } else {
-                        BitRecorder rec{lds_u[j & 1u], lds_d[j & 1u], col};
+                        BitRecorder<STATS> rec{lds_u[j & 1u], lds_d[j & 1u], col};
                         core.run(a.t0 + k0, steps, rec);
                         rec.flush();
+                        counts = rec.cnt.packed;
+                    }
+                }
+                if (STATS) {
+                    // a wave's sums of the 10-bit fields fit 16 bits (64 x 512)
+                    const uint32_t lo = wave_sum((counts & 1023u) | (((counts >> 10) & 1023u) << 16));
+                    const uint32_t hi = wave_sum(counts >> 20);
+                    if (lane == 0u) {
+                        atomicAdd(&blk_stats[m & 1u][0], lo & 0xFFFFu);
+                        atomicAdd(&blk_stats[m & 1u][2], lo >> 16);
+                        atomicAdd(&blk_stats[m & 1u][3], hi);
                     }
                 }
                 if (r + 1u == rounds) {
                     if (live) core.store(a);
                     if (STATS) {
-                        const uint32_t v0 = wave_sum(live ? core.n_eps : 0u);
-                        const uint32_t v1 = wave_sum(live ? core.finished_length_sum(a.K) : 0u);
-                        const uint32_t v2 = wave_sum(live ? core.n_term : 0u);
-                        const uint32_t v3 = wave_sum(live ? core.n_trunc : 0u);
-                        if (lane == 0u) {
-                            atomicAdd(&blk_stats[m & 1u][0], v0);
-                            atomicAdd(&blk_stats[m & 1u][1], v1);
-                            atomicAdd(&blk_stats[m & 1u][2], v2);
-                            atomicAdd(&blk_stats[m & 1u][3], v3);
-                        }
+                        const uint32_t e1 = wave_sum(live ? core.ep : 0u);
+                        if (lane == 0u) atomicAdd(&blk_stats[m & 1u][1], 0u - e1);
                     }
                 }
-                // with one word per lane the stepping waves join the replay only
+                // up to 8 words per lane the stepping waves join the replay only
                 // after their last item: their cart-pole state and the replay's
-                // words then never share registers, which keeps the kernel at
-                // eight waves per SIMD, two workgroups per CU, without spills
-                if (W != 1 && j >= 1u) replay_item(j - 1u);
+                // words then never share registers, which keeps the kernel within
+                // the 64 VGPRs of eight waves per SIMD, two workgroups per CU
+                if (W > 8 && j >= 1u) replay_item(j - 1u);
                 __syncthreads();
             }
         }

@@ -53,8 +53,12 @@ def test_jump_tables_have_the_layout_the_replay_jumps_into(tmp_path):
                 k += 1
             assert ins[k][1] == "s_setpc_b64 s[44:45]" and ins[k][2] == 4, (uid, leaf, ins[k])
             k += 1
-    muls = {t for _, t, _ in ins if re.match(r"s_mul_i32 s40, s40,", t)}
-    assert muls == {f"s_mul_i32 s40, s40, {LEAF_BYTES:#x}"}, muls
-    # every step's call, and every stub's call of the clearing routine, as many as the tables need
-    calls = [t for _, t, _ in ins if t.startswith("s_swappc_b64 s[44:45], ")]
-    assert len(calls) == len(tables) * 4 * 32, (len(calls), len(tables))
+    # within each replay block (from its prologue to its end label): every index
+    # multiply is by 68, and there are as many calls as its steps and stubs make
+    for uid in tables:
+        lo, hi = labels["Ljbase0_" + uid], labels["Ljend" + uid]
+        body = [t for a, t, _ in ins if lo <= a < hi]
+        muls = {t for t in body if t.startswith("s_mul_i32 ")}
+        assert muls == {f"s_mul_i32 s40, s40, {LEAF_BYTES:#x}"}, (uid, muls)
+        calls = [t for t in body if t.startswith("s_swappc_b64 s[44:45], ")]
+        assert len(calls) == 4 * 32, (uid, len(calls))
