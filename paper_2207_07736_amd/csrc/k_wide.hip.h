@@ -348,21 +348,25 @@ __device__ __forceinline__ void replay_env(const StepArgs& a, const uint32_t* ld
     const uint32_t chunk_words = 64u * W;
     const uint32_t n_chunks = (a.Dp + chunk_words - 1u) / chunk_words;
     const uint32_t env = blk * kBlock + col;
-    const bool live = env < a.n;
+    const size_t row = (size_t)env * a.Dp;
+    const uint32_t words = env < a.n ? a.Dp : 0u;
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(a.pad_s + row, words), ra = row_rsrc(a.pad_a + row, words),
+                                 rb = row_rsrc(a.pad_b + row, words);
     for (uint32_t c = 0; c < n_chunks; ++c) {
         const uint32_t base = c * chunk_words + 4u * lane;
         float s[W], pa[W], pb[W];
-        const size_t row = (size_t)env * a.Dp;
 #pragma unroll
         for (int i = 0; i < W; i += 4) {
-            const uint32_t j = base + (uint32_t)(i / 4) * 256u;
-            const bool on = live && j < a.Dp;
-            const float4 vs = on ? *reinterpret_cast<const float4*>(a.pad_s + row + j) : float4{0, 0, 0, 0};
-            const float4 va = on ? *reinterpret_cast<const float4*>(a.pad_a + row + j) : float4{0, 0, 0, 0};
-            const float4 vb = on ? *reinterpret_cast<const float4*>(a.pad_b + row + j) : float4{0, 0, 0, 0};
-            s[i] = vs.x; s[i + 1] = vs.y; s[i + 2] = vs.z; s[i + 3] = vs.w;
-            pa[i] = va.x; pa[i + 1] = va.y; pa[i + 2] = va.z; pa[i + 3] = va.w;
-            pb[i] = vb.x; pb[i + 1] = vb.y; pb[i + 2] = vb.z; pb[i + 3] = vb.w;
+            const uint32_t jb = 4u * (base + (uint32_t)(i / 4) * 256u);
+            const u32x4 vs = __builtin_amdgcn_raw_buffer_load_b128(rs, jb, 0, 0);
+            const u32x4 va = __builtin_amdgcn_raw_buffer_load_b128(ra, jb, 0, 0);
+            const u32x4 vb = __builtin_amdgcn_raw_buffer_load_b128(rb, jb, 0, 0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                s[i + q] = __uint_as_float(vs[q]);
+                pa[i + q] = __uint_as_float(va[q]);
+                pb[i + q] = __uint_as_float(vb[q]);
+            }
         }
         for (uint32_t w32 = 0; w32 * 32u < steps; ++w32) {
             const uint32_t ub = lds_u[w32 * kBlock + col];
@@ -373,9 +377,10 @@ __device__ __forceinline__ void replay_env(const StepArgs& a, const uint32_t* ld
         }
 #pragma unroll
         for (int i = 0; i < W; i += 4) {
-            const uint32_t j = base + (uint32_t)(i / 4) * 256u;
-            if (live && j < a.Dp)
-                *reinterpret_cast<float4*>(a.pad_s + row + j) = float4{s[i], s[i + 1], s[i + 2], s[i + 3]};
+            const uint32_t jb = 4u * (base + (uint32_t)(i / 4) * 256u);
+            const u32x4 v = {__float_as_uint(s[i]), __float_as_uint(s[i + 1]), __float_as_uint(s[i + 2]),
+                             __float_as_uint(s[i + 3])};
+            __builtin_amdgcn_raw_buffer_store_b128(v, rs, jb, 0, 0);
         }
     }
 }
@@ -538,26 +543,25 @@ __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t
 }
 
 // k_cartpole_wide<W, E, NW>: the two phases, overlapped across the blocks of a
-// persistent workgroup of NW waves (one workgroup per CU; workgroup g takes the
-// 256-env blocks g, g + G, ... of a grid of G).  A work item is one 512-step
-// round of one block, and the workgroup's items are its blocks round by round.
-// In iteration j the first four waves run phase 1 of item j (the cart-pole loop
-// with its trajectory stores, the action and done bits into LDS slot j & 1) and
-// then help replay item j - 1; the other waves replay item j - 1 from slot
-// (j - 1) & 1, taking E-environment groups from an LDS counter; one workgroup
-// barrier ends the iteration.  Phase 1 of one block thus runs beside the replay
+// persistent workgroup of NW waves (one or two workgroups per CU; workgroup g
+// takes the 256-env blocks g, g + G, ... of a grid of G).  A work item is one
+// 512-step round of one block, and the workgroup's items are its blocks round
+// by round.  In iteration j the first four waves run phase 1 of item j (the
+// cart-pole loop with its trajectory stores, the action and done bits into LDS
+// slot j & 1) and, for W = 64, then help replay item j - 1; the other waves
+// replay item j - 1 from slot (j - 1) & 1, taking E-environment groups from an
+// LDS counter; one workgroup barrier ends the iteration.  Phase 1 of one block thus runs beside the replay
 // of the one before it, and only the first item's phase 1 is exposed (262,144
 // envs x 500 steps against the same phases run one after the other in 256-env
 // workgroups: D = 512 2.11 against 2.45 ms, D = 2,048 6.33 against 8.59 ms).
 // Block statistics go through LDS slot m & 1 of the workgroup's m-th block and
 // are written out by wave 4 in the iteration after the block's last item.
-// With one word per lane (the jump-table replay, bound by the latency of its
-// jumps rather than by issue) two workgroups run per CU, eight waves per SIMD:
-// D = 64 0.88-0.93 against 0.99-1.05 ms with one.  There the stepping waves
-// join the replay only after the workgroup's last item, which keeps the kernel
-// within the 64 VGPRs that eight waves per SIMD allow, without spills.
+// Up to 16 words per lane two workgroups run per CU, eight waves per SIMD:
+// the replay's scalar bit tests and branches, not its vector updates, set its
+// pace, and more waves hide more of them (D = 64 0.88-0.93 against 0.99-1.05 ms
+// with one workgroup, D = 512 2.00-2.04 against 2.17-2.29 ms).
 template <int W, int E, int NW, bool REC, bool STATS>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W <= 8 ? 8 : 1)))
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W <= 16 ? 8 : W == 32 ? 4 : 1)))
 void k_cartpole_wide(StepArgs a)
 {
     static_assert(NW >= 8 && NW <= 16, "the pipeline needs four stepping waves and at least four more");
@@ -659,11 +663,12 @@ void k_cartpole_wide(StepArgs a)
                         if (lane == 0u) atomicAdd(&blk_stats[m & 1u][1], 0u - e1);
                     }
                 }
-                // up to 8 words per lane the stepping waves join the replay only
+                // up to 32 words per lane the stepping waves join the replay only
                 // after their last item: their cart-pole state and the replay's
                 // words then never share registers, which keeps the kernel within
-                // the 64 VGPRs of eight waves per SIMD, two workgroups per CU
-                if (W > 8 && j >= 1u) replay_item(j - 1u);
+                // the 64 VGPRs of eight waves per SIMD (two workgroups per CU) up
+                // to 16 words, and within the 128 of four up to 32
+                if (W > 32 && j >= 1u) replay_item(j - 1u);
                 __syncthreads();
             }
         }

@@ -244,17 +244,16 @@ hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s
         // E = 2 5.0 against E = 1 3.94 ms: four environments of 8 words, or two
         // of 16, take the kernel past 128 VGPRs and below four waves per SIMD).
         // Up to 64 words: one word per lane, eight environments per step
-        // through the replay's jump table.  Up to 8 words per lane (D <= 512)
+        // through the replay's jump table.  Up to 16 words per lane (D <= 1,024)
         // the kernel fits the 64 VGPRs of eight waves per SIMD, and two
-        // persistent 16-wave workgroups run per CU; above, one per CU, of as
-        // many waves as the replay's registers allow four of per SIMD (three for
-        // W = 32, two for W = 64).
+        // persistent 16-wave workgroups run per CU; above, one per CU: 16 waves
+        // (four per SIMD, 115 VGPRs) for W = 32, 8 for W = 64.
         const dim3 pgrid(min(grid_for(a.n), cus)), pgrid2(min(grid_for(a.n), 2u * cus));
         if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
         else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
         else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
-        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
-        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, 1, 12, REC, STATS>), pgrid, dim3(768), 0, s, a);
+        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
+        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
         else hipLaunchKernelGGL((k_cartpole_wide<64, 1, 8, REC, STATS>), pgrid, dim3(512), 0, s, a);
     }
     return hipGetLastError();
