@@ -28,12 +28,10 @@ import workloads  # noqa: E402
 METRIC = "env-steps/sec at 1 MI355X; achieved HBM GB/s vs peak; fused/unfused speedup"
 HBM_PEAK_GBS = 8000.0
 # fp32 VALU peak in lane operations (one FMA or multiply per lane) per second:
-# the published 157.3 TFLOP/s fp32 vector rate, an FMA counted as two flops.
-# That figure counts two FMAs per lane per cycle, which only packed fp32
-# instructions reach; the kernels use none.  Plain v_fma_f32 issues at half of
-# it (3.83e13 lane-ops/s measured by rlsim_probe_issue at eight waves per SIMD,
-# a four-cycle wave64 issue), v_mul_f32 at 6.3e13, so a padding replay with
-# random actions (half FMAs, half multiplies) is capped near 0.61 of this peak.
+# the published 157.3 TFLOP/s fp32 vector rate, an FMA counted as two flops,
+# i.e. 32 lanes per clock per SIMD at 2.4 GHz.  Plain (non-packed) v_fma_f32 and
+# v_mul_f32 reach 25-29.5 lanes per clock (rlsim_probe_issue, eight waves per
+# SIMD); under sustained VALU load the shader clock falls to 1.6-2.2 GHz.
 VALU_LANE_OPS_PER_S = 157.3e12 / 2
 COPY_BYTES = 1 << 30        # size of the plain copy used to calibrate the HBM byte counters
 

@@ -53,20 +53,21 @@ def test_wide_long_launch_crosses_chunks(D):
     assert_bit_equal(g, r)
 
 
-@pytest.mark.parametrize("D", [48, 72, 300, 1100])
+@pytest.mark.parametrize("D", [48, 72, 300, 700, 1100])
 def test_wide_pipeline_several_blocks_per_workgroup(D):
-    """More 256-env blocks than the persistent grid has workgroups (one per CU):
-    workgroup 0 runs blocks 0 and 256 one after the other, the last block is
-    partial, and K = 800 takes two 512-step rounds per block, so several items
-    of one block pass through the pipeline; a second call of K = 300 follows.
-    The columns of blocks 0, 256 and the partial last one -- the trajectory,
-    the cart-pole state and every padding word -- and their statistics rows
-    equal the oracle's slices at the same global ids (D = 48, 72, 300 and 1,100
-    take the jump-table, 4-, 8- and 32-words-per-lane shapes, of 16, 16, 16 and
-    12 waves)."""
-    n = 256 * 257 + 100
+    """More 256-env blocks than the persistent grid has workgroups (two per CU
+    up to 16 words per lane, one above; 256 CUs): 514 blocks, the last one
+    partial, so workgroup 0 runs blocks 0 and 512 (0, 256 and 512 on the
+    one-per-CU grid) one after the other, and K = 800 takes two 512-step rounds
+    per block, so several items of one block pass through the pipeline; a second
+    call of K = 300 follows.  The columns of blocks 0, 256, 512 and the partial
+    last one -- the trajectory, the cart-pole state and every padding word --
+    and their statistics rows equal the oracle's slices at the same global ids
+    (D = 48, 72, 300, 700 and 1,100 take the jump-table, 4-, 8-, 16- and
+    32-words-per-lane shapes)."""
+    n = 256 * 513 + 100
     T, sched = 1100, [800, 300]
-    slices = [(0, 256), (256 * 256, 256 * 257), (256 * 257, n)]
+    slices = [(0, 256), (256 * 256, 256 * 257), (256 * 512, 256 * 513), (256 * 513, n)]
     print(f"wide pipeline D={D} n={n} sched={sched}", flush=True)
     g = gpu_run(n, T, sched, D=D, seed=21, slices=slices)
     refs = [oracle_run(b - a, T, sched, D=D, seed=21, env0=a) for a, b in slices]
@@ -85,9 +86,10 @@ def test_wide_pipeline_without_trajectory(D):
     """The wide kernel's forms without a trajectory, at the multi-block size of
     the test above: a call with traj = NULL and a statistics-only call leave the
     same state as the recording call, the statistics equal the recording call's,
-    and both match the oracle's slices of the first and last blocks."""
+    and both match the oracle's slices of the first block, of block 512 (the
+    second block of workgroup 0 on the two-per-CU grid) and of the last block."""
     from paper_2207_07736_amd import Simulator, Trajectory, stats_only
-    n, T, seed = 256 * 257 + 100, 700, 23
+    n, T, seed = 256 * 513 + 100, 700, 23
     states, stats = [], []
     for form in ("traj", "none", "stats"):
         sim = Simulator(n, D, workloads.CARTPOLE)
@@ -112,7 +114,7 @@ def test_wide_pipeline_without_trajectory(D):
         assert np.array_equal(st.view(np.uint32), states[0][0].view(np.uint32))
         assert np.array_equal(ep, states[0][1]) and t == T
     assert torch.equal(stats[0], stats[1])
-    for a, b in ((0, 256), (256 * 257, n)):
+    for a, b in ((0, 256), (256 * 512, 256 * 513), (256 * 513, n)):
         r = oracle_run(b - a, T, [T], D=D, seed=seed, env0=a)
         assert np.array_equal(states[0][0][:, a:b].view(np.uint32), r["state"].view(np.uint32))
         assert np.array_equal(stats[1].cpu().numpy().view(np.uint32)[a // 256:a // 256 + len(r["stats"][0])],
