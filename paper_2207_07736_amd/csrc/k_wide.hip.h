@@ -67,7 +67,7 @@ struct BitRecorder {
 };
 
 // Wave-uniform replay of the padding recurrence (one environment per wave, so
-// the action and done bits are scalars): for N words of this lane at offset O,
+// the action and done bits are scalars): for the 16 words of this lane,
 // run steps 0 .. m-1 of one 32-step bit word as a scalar loop around in-place
 // VALU updates, i.e. one vector instruction per word per step.  Each step is
 //   bit u set:   s <- fma(a, s, b)     (one rounding, v_fma_f32)
@@ -82,11 +82,6 @@ struct BitRecorder {
 #define RL_REP4(X) X(0) X(1) X(2) X(3)
 #define RL_REP8(X) RL_REP4(X) X(4) X(5) X(6) X(7)
 #define RL_REP16(X) RL_REP8(X) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15)
-#define RL_REP32(X) \
-    RL_REP16(X) X(16) X(17) X(18) X(19) X(20) X(21) X(22) X(23) X(24) X(25) X(26) X(27) X(28) X(29) X(30) X(31)
-#define RL_REP64(X)                                                                                      \
-    RL_REP32(X) X(32) X(33) X(34) X(35) X(36) X(37) X(38) X(39) X(40) X(41) X(42) X(43) X(44) X(45) X(46) \
-        X(47) X(48) X(49) X(50) X(51) X(52) X(53) X(54) X(55) X(56) X(57) X(58) X(59) X(60) X(61) X(62) X(63)
 #define RL_FMA(i) "v_fma_f32 %[s" #i "], %[a" #i "], %[s" #i "], %[b" #i "]\n"
 #define RL_MUL(i) "v_mul_f32 %[s" #i "], %[a" #i "], %[s" #i "]\n"
 #define RL_ZERO(i) "v_mov_b32 %[s" #i "], 0\n"
@@ -115,31 +110,15 @@ struct BitRecorder {
                  : REP(RL_IN_A) REP(RL_IN_B)[ub] "s"(ub), [db] "s"(db), [m] "s"(m)       \
                  : "scc")
 
-template <int N, int O, int W>
-__device__ __forceinline__ void replay_uniform_group(float (&s)[W], const float (&pa)[W], const float (&pb)[W],
-                                                     uint32_t ub, uint32_t db, uint32_t m)
-{
-    static_assert(O + N <= W, "group outside the lane's words");
-    uint32_t cnt;
-    if constexpr (N == 64) RL_REPLAY_ASM(RL_REP64);
-    else if constexpr (N == 32) RL_REPLAY_ASM(RL_REP32);
-    else if constexpr (N == 16) RL_REPLAY_ASM(RL_REP16);
-    else if constexpr (N == 8) RL_REPLAY_ASM(RL_REP8);
-    else RL_REPLAY_ASM(RL_REP4);
-}
-
-// All W words of the lane, in groups of at most kReplayGroup.
-constexpr int kReplayGroup = 64;
-template <int W, int O = 0>
+// All 16 words of the lane in one asm block.
+template <int W>
 __device__ __forceinline__ void replay_uniform(float (&s)[W], const float (&pa)[W], const float (&pb)[W],
                                                uint32_t ub, uint32_t db, uint32_t m)
 {
-    if constexpr (O < W) {
-        constexpr int R = W - O;
-        constexpr int N = R >= kReplayGroup ? kReplayGroup : R >= 32 ? 32 : R >= 16 ? 16 : R >= 8 ? 8 : 4;
-        replay_uniform_group<N, O, W>(s, pa, pb, ub, db, m);
-        replay_uniform<W, O + N>(s, pa, pb, ub, db, m);
-    }
+    static_assert(W == 16, "the one-environment replay holds 16 words per lane");
+    constexpr int O = 0;
+    uint32_t cnt;
+    RL_REPLAY_ASM(RL_REP16);
 }
 
 // The same replay for E environments at once (E = 2 or 4): each lane holds W
@@ -543,28 +522,31 @@ __device__ __forceinline__ void replay_group_jt(const StepArgs& a, const uint8_t
 }
 
 // k_cartpole_wide<W, E, NW>: the two phases, overlapped across the blocks of a
-// persistent workgroup of NW waves (one or two workgroups per CU; workgroup g
-// takes the 256-env blocks g, g + G, ... of a grid of G).  A work item is one
-// 512-step round of one block, and the workgroup's items are its blocks round
-// by round.  In iteration j the first four waves run phase 1 of item j (the
-// cart-pole loop with its trajectory stores, the action and done bits into LDS
-// slot j & 1) and, for W = 64, then help replay item j - 1; the other waves
-// replay item j - 1 from slot (j - 1) & 1, taking E-environment groups from an
-// LDS counter; one workgroup barrier ends the iteration.  Phase 1 of one block thus runs beside the replay
+// persistent workgroup of NW waves (two workgroups per CU; workgroup g takes
+// the 256-env blocks g, g + G, ... of a grid of G).  A work item is one 512-step
+// round of one block, and the workgroup's items are its blocks round by round.
+// In iteration j the first four waves run phase 1 of item j (the cart-pole loop
+// with its trajectory stores, the action and done bits into LDS slot j & 1);
+// the other waves replay item j - 1 from slot (j - 1) & 1, taking
+// E-environment groups from an LDS counter; one workgroup barrier ends the
+// iteration.  The stepping waves join the replay after the workgroup's last
+// item: their cart-pole state and the replay's words then never share
+// registers, which keeps the kernel within the 64 VGPRs of eight waves per SIMD.  Phase 1 of one block thus runs beside the replay
 // of the one before it, and only the first item's phase 1 is exposed (262,144
 // envs x 500 steps against the same phases run one after the other in 256-env
 // workgroups: D = 512 2.11 against 2.45 ms, D = 2,048 6.33 against 8.59 ms).
 // Block statistics go through LDS slot m & 1 of the workgroup's m-th block and
 // are written out by wave 4 in the iteration after the block's last item.
-// Up to 16 words per lane two workgroups run per CU, eight waves per SIMD:
-// the replay's scalar bit tests and branches, not its vector updates, set its
-// pace, and more waves hide more of them (D = 64 0.88-0.93 against 0.99-1.05 ms
-// with one workgroup, D = 512 2.00-2.04 against 2.17-2.29 ms).
+// Two workgroups run per CU, eight waves per SIMD: the replay's scalar bit
+// tests and branches, not its vector updates, set its pace, and more waves
+// hide more of them (D = 64 0.88-0.93 against 0.99-1.05 ms with one workgroup,
+// D = 512 2.00-2.04 against 2.17-2.29 ms).
 template <int W, int E, int NW, bool REC, bool STATS>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(W <= 16 ? 8 : W == 32 ? 4 : 1)))
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(8)))
 void k_cartpole_wide(StepArgs a)
 {
     static_assert(NW >= 8 && NW <= 16, "the pipeline needs four stepping waves and at least four more");
+    static_assert(W == 1 || W == 4 || W == 8 || W == 16, "shapes that fit 64 VGPRs");
     static_assert(W != 1 || E == (int)kJtGroup, "one word per lane takes the eight-environment jump table");
     __shared__ uint32_t lds_u[2][kChunkWords * kBlock];
     __shared__ uint32_t lds_d[2][kChunkWords * kBlock];
@@ -609,7 +591,7 @@ void k_cartpole_wide(StepArgs a)
 
     if (wave < 4u) {
         // stepping waves: phase 1 of every item, in order, then their share of
-        // the previous item's replay
+        // the last item's replay
         const uint32_t col = threadIdx.x;
         uint32_t j = 0u;
         for (uint32_t m = 0; m < my_blocks; ++m) {
@@ -663,12 +645,6 @@ void k_cartpole_wide(StepArgs a)
                         if (lane == 0u) atomicAdd(&blk_stats[m & 1u][1], 0u - e1);
                     }
                 }
-                // up to 32 words per lane the stepping waves join the replay only
-                // after their last item: their cart-pole state and the replay's
-                // words then never share registers, which keeps the kernel within
-                // the 64 VGPRs of eight waves per SIMD (two workgroups per CU) up
-                // to 16 words, and within the 128 of four up to 32
-                if (W > 32 && j >= 1u) replay_item(j - 1u);
                 __syncthreads();
             }
         }

@@ -240,21 +240,20 @@ hipError_t launch_step(const StepArgs& a, bool wide, uint32_t cus, hipStream_t s
         // one environment per wave in the replay (wave-uniform bits), W words
         // per lane; E environments replayed together where that pays
         // (262,144 envs x 500 steps, phases not overlapped: D = 256 1.84 / 1.98 /
-        // 2.24 ms for E = 4 / 2 / 1, D = 512 3.10 / 2.55 / 2.81 ms, D = 1,024
-        // E = 2 5.0 against E = 1 3.94 ms: four environments of 8 words, or two
-        // of 16, take the kernel past 128 VGPRs and below four waves per SIMD).
-        // Up to 64 words: one word per lane, eight environments per step
-        // through the replay's jump table.  Up to 16 words per lane (D <= 1,024)
-        // the kernel fits the 64 VGPRs of eight waves per SIMD, and two
-        // persistent 16-wave workgroups run per CU; above, one per CU: 16 waves
-        // (four per SIMD, 115 VGPRs) for W = 32, 8 for W = 64.
-        const dim3 pgrid(min(grid_for(a.n), cus)), pgrid2(min(grid_for(a.n), 2u * cus));
-        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
-        else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
-        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
-        else if (a.D <= 1024u) hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), pgrid2, dim3(1024), 0, s, a);
-        else if (a.D <= 2048u) hipLaunchKernelGGL((k_cartpole_wide<32, 1, 16, REC, STATS>), pgrid, dim3(1024), 0, s, a);
-        else hipLaunchKernelGGL((k_cartpole_wide<64, 1, 8, REC, STATS>), pgrid, dim3(512), 0, s, a);
+        // 2.24 ms for E = 4 / 2 / 1, D = 512 3.10 / 2.55 / 2.81 ms).  Up to 64
+        // words: one word per lane, eight environments per step through the
+        // replay's jump table.  Above 512 words, 16 words per lane in chunks of
+        // 1,024 (D = 2,048 / 4,096 / 5,000: 5.90-5.92 / 11.16-11.20 /
+        // 13.84-13.85 ms against 6.01-6.10 / 11.61 / 16.4 ms with 32 words per
+        // lane at four waves per SIMD, whose 2,048-word chunks waste more of the
+        // last one, and 11.9-12.4 ms at D = 4,096 with 64 words at two waves).
+        // Every shape fits the 64 VGPRs of eight waves per SIMD: two persistent
+        // 16-wave workgroups per CU.
+        const dim3 grid2(min(grid_for(a.n), 2u * cus)), block2(1024);
+        if (a.D <= 64u) hipLaunchKernelGGL((k_cartpole_wide<1, 8, 16, REC, STATS>), grid2, block2, 0, s, a);
+        else if (a.D <= 256u) hipLaunchKernelGGL((k_cartpole_wide<4, 4, 16, REC, STATS>), grid2, block2, 0, s, a);
+        else if (a.D <= 512u) hipLaunchKernelGGL((k_cartpole_wide<8, 2, 16, REC, STATS>), grid2, block2, 0, s, a);
+        else hipLaunchKernelGGL((k_cartpole_wide<16, 1, 16, REC, STATS>), grid2, block2, 0, s, a);
     }
     return hipGetLastError();
 }

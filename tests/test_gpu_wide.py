@@ -27,10 +27,10 @@ def _need_gpu():
 
 
 # D values cover every kernel shape: register-resident words (<= 32), one word
-# per lane for eight envs at a time (33-64), one env per wave with
-# 4/8/16/32/64 words per lane (four or two envs per scalar decision up to 512
-# words), ragged rows (D not a multiple of 4 or of the chunk) and several word
-# chunks per env (D > 4096).
+# per lane for eight envs at a time (33-64), 4/8/16 words per lane (four or two
+# envs per scalar decision up to 512 words, one above), ragged rows (D not a
+# multiple of 4 or of the chunk) and several 1,024-word chunks per env
+# (D > 1,024).
 @pytest.mark.parametrize("D", [17, 32, 33, 63, 64, 65, 100, 256, 512, 777, 1024, 2048, 4096, 5000])
 def test_wide_padding_bit_exact(D):
     n = 260                                   # two stats blocks, ragged tail
@@ -56,15 +56,14 @@ def test_wide_long_launch_crosses_chunks(D):
 @pytest.mark.parametrize("D", [48, 72, 300, 700, 1100])
 def test_wide_pipeline_several_blocks_per_workgroup(D):
     """More 256-env blocks than the persistent grid has workgroups (two per CU
-    up to 16 words per lane, one above; 256 CUs): 514 blocks, the last one
-    partial, so workgroup 0 runs blocks 0 and 512 (0, 256 and 512 on the
-    one-per-CU grid) one after the other, and K = 800 takes two 512-step rounds
+    on 256 CUs): 514 blocks, the last one partial, so workgroup 0 runs blocks 0
+    and 512 one after the other, and K = 800 takes two 512-step rounds
     per block, so several items of one block pass through the pipeline; a second
     call of K = 300 follows.  The columns of blocks 0, 256, 512 and the partial
     last one -- the trajectory, the cart-pole state and every padding word --
     and their statistics rows equal the oracle's slices at the same global ids
-    (D = 48, 72, 300, 700 and 1,100 take the jump-table, 4-, 8-, 16- and
-    32-words-per-lane shapes)."""
+    (D = 48, 72, 300, 700 and 1,100 take the jump-table, 4-, 8- and
+    16-words-per-lane shapes, the last in two 1,024-word chunks)."""
     n = 256 * 513 + 100
     T, sched = 1100, [800, 300]
     slices = [(0, 256), (256 * 256, 256 * 257), (256 * 512, 256 * 513), (256 * 513, n)]
