@@ -43,6 +43,22 @@ def test_wide_padding_bit_exact(D):
         assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("n", [1, 63, 65])
+@pytest.mark.parametrize("D", [48, 300, 1100])
+def test_wide_tiny_populations(n, D):
+    """A grid of one persistent workgroup whose only block is partial (one env,
+    a partial wave, a wave and one lane), for the jump-table, 8- and
+    16-words-per-lane shapes: trajectory, state, every padding word and the
+    statistics row equal the oracle's."""
+    T = 300
+    sched = [37, T - 37]
+    g = gpu_run(n, T, sched, D=D, seed=11)
+    r = oracle_run(n, T, sched, D=D, seed=11)
+    assert_bit_equal(g, r)
+    for a, b in zip(g["stats"], r["stats"]):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("D", [20, 64, 512])
 def test_wide_long_launch_crosses_chunks(D):
     """K larger than the 512-step LDS round: the padding words are carried over
